@@ -1,0 +1,179 @@
+/*
+ * mcd.h -- C ABI of libmcd, the MI355X (gfx950) multi-codebook audio decode head.
+ *
+ * One decode step of the output stage of a delay-pattern speech LM served with
+ * paired classifier-free guidance (arXiv 2607.02119):
+ *   - K codebook head projections of every row's hidden state (Sec. 2.1: each
+ *     of the S parallel heads maps h_t to its logits; head k is the k-th audio
+ *     slice of the shared head, its stream-embedding term folds into a bias);
+ *   - the in-batch CFG merge of each conditional (Main) row with its
+ *     unconditional (Companion) partner, w * l_cond + (1 - w) * l_uncond, per
+ *     codebook (Eq. 1), only for audio rows (Sec. 2.4);
+ *   - temperature, top-k and top-p selection and a Gumbel-max draw keyed by a
+ *     counter-based Philox4x64-10 generator, for all K streams of a row in the
+ *     same step (synchronous multi-stream sampling, Sec. 2.3);
+ *   - the delay pattern: codebook k at step t carries frame t - d_k (Sec. 2.1);
+ *     positions with no frame (before the stream starts, or in the drain that
+ *     flushes the last S-1 steps, Sec. 2.3) carry the pad id;
+ *   - the sampled Main token copied to the Companion row, whose own outputs
+ *     stay hidden (Sec. 2.4), and each frame scattered into a per-request
+ *     frame grid (the de-interleaved S x T codebook matrix, Sec. 2.1 / 2.3).
+ *
+ * Conventions
+ *   - Pointers are DEVICE pointers unless marked [host].  Every buffer is owned
+ *     by the caller; the library never allocates device memory, never
+ *     synchronises (except mcd_read_device_status) and launches only on the
+ *     stream it is given.
+ *   - Row-major layouts; sizes in elements unless named *_bytes.
+ *   - Errors: argument and shape errors return MCD_E_INVALID or
+ *     MCD_E_UNSUPPORTED before anything is launched; a failed launch returns
+ *     MCD_E_HIP.  mcd_last_error() gives a thread-local description of the last
+ *     non-OK return.  No call aborts or throws.  Conditions only the device can
+ *     see (a parameter value out of range, a grid cell outside the grid, a
+ *     corrupt plan) set bits of a sticky status word in the workspace and make
+ *     the affected outputs the pad id; read it with mcd_read_device_status.
+ *   - Calls that share a workspace must not overlap in time.
+ */
+#ifndef MCD_H
+#define MCD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MCD_OK = 0,
+  MCD_E_INVALID = 1,      /* bad argument, shape or batch structure */
+  MCD_E_UNSUPPORTED = 2,  /* valid but outside what the kernels implement */
+  MCD_E_WORKSPACE = 3,    /* workspace missing or too small */
+  MCD_E_HIP = 4           /* the HIP runtime reported an error */
+} mcd_status;
+
+typedef enum { MCD_F32 = 0, MCD_BF16 = 1 } mcd_dtype;
+
+/* Row kinds of a continuous batch (Sec. 2.4: a Main request with CFG scale
+ * w > 1 gets a Companion; both are scheduled together). */
+enum { MCD_ROW_COND = 0, MCD_ROW_UNCOND = 1, MCD_ROW_SOLO = 2, MCD_ROW_TEXT = 3 };
+
+/* Bits of the device status word. */
+enum {
+  MCD_DEV_BAD_PARAM = 1u,   /* temperature < 0 or NaN, top_p <= 0 or NaN, non-finite w */
+  MCD_DEV_GRID_RANGE = 2u,  /* grid_slot >= n_slots or frame >= F_max: cell not written */
+  MCD_DEV_BAD_PLAN = 4u     /* device plan does not match the counts of the call */
+};
+
+#define MCD_MAX_K 32         /* codebooks per head */
+#define MCD_MAX_V 4096       /* audio sub-vocabulary size per codebook */
+
+typedef struct mcd_head mcd_head;   /* opaque, immutable after creation, thread-safe */
+
+/* Head description.  The weights are borrowed: they must stay valid and
+ * unchanged while the handle is used. */
+typedef struct {
+  int32_t H;                 /* hidden size; multiple of 64 for MCD_BF16, of 4 for MCD_F32 */
+  int32_t K;                 /* codebooks (streams), 1..MCD_MAX_K */
+  int32_t V;                 /* audio sub-vocabulary per codebook, 1..MCD_MAX_V */
+  int32_t pad_id;            /* token emitted where the delay pattern has no frame */
+  const int32_t *delays;     /* [host][K] d_k >= 0; copied at creation */
+  mcd_dtype dtype;           /* element type of hidden, W and W_text */
+  const void *W;             /* [K][V][H]: row n = k*V + v is head k's weight for id v */
+  const float *bias;         /* [K][V] or NULL: stream-embedding term W_k e_k */
+  int32_t V_text;            /* text vocabulary of the text head, 0 if none */
+  const void *W_text;        /* [V_text][H] or NULL */
+} mcd_head_desc;
+
+mcd_status mcd_head_create(const mcd_head_desc *desc, mcd_head **out);
+void mcd_head_destroy(mcd_head *head);
+
+/* ---- batch plan -----------------------------------------------------------
+ * Built on the host once per batch composition (not per step) from the pair
+ * map and row kinds, then copied to device memory by the caller.
+ *   pair_map[r]: partner row of a COND or UNCOND row, -1 for SOLO and TEXT rows;
+ *   partners must point at each other and be one COND and one UNCOND row.
+ * The plan fixes the "sampled order" of audio rows: the Main rows of the pairs
+ * in ascending row order, then the SOLO rows in ascending row order.  Scores
+ * are laid out in that order (see mcd_step_args.scores). */
+typedef struct {
+  int32_t n_pairs, n_solo, n_text;
+} mcd_batch_counts;
+
+size_t mcd_plan_words(int32_t R);   /* int32 words of a plan for R rows */
+
+/* [host] Validate the batch and write the plan.  No HIP call.  Fails with
+ * MCD_E_INVALID (and writes nothing) for an inconsistent pair map, an unknown
+ * row kind, or TEXT rows on a head without a text head. */
+mcd_status mcd_batch_plan(const mcd_head *head, int32_t R, const int32_t *pair_map,
+                          const uint8_t *row_kind, int32_t *plan, size_t plan_words,
+                          mcd_batch_counts *counts);
+
+/* [host] Physical row of sampled index s (0 <= s < n_pairs + n_solo) and its
+ * companion row (-1 for a SOLO row), read from a host copy of the plan. */
+mcd_status mcd_plan_sampled_row(const int32_t *plan, int32_t s, int32_t *row, int32_t *companion);
+
+/* Workspace bytes for a batch of up to R rows; the workspace must be 256-byte
+ * aligned and zero-filled once before first use (the status word lives in it). */
+size_t mcd_workspace_bytes(const mcd_head *head, int32_t R);
+
+/* ---- one decode step -----------------------------------------------------*/
+typedef struct {
+  int32_t R;                 /* rows in the batch */
+  mcd_batch_counts counts;   /* as returned by mcd_batch_plan */
+  const int32_t *plan;       /* device copy of the plan words */
+  const void *hidden;        /* [R][H] of the head's dtype, 16-byte aligned */
+  const float *cfg_w;        /* [R] CFG scale, read on COND rows (any finite w) */
+  const float *temperature;  /* [R] >= 0; 0 selects greedy decoding */
+  const int32_t *top_k;      /* [R] <= 0 or >= V: no top-k */
+  const float *top_p;        /* [R] in (0, 1); >= 1: no top-p */
+  const uint64_t *rng_key;   /* [R] stable request id (Main row's for a pair), or NULL: row index */
+  const int32_t *step;       /* [R] decode step t of the row */
+  const int32_t *n_frames;   /* [R] frames of the request, -1 if open-ended */
+  const int32_t *grid_slot;  /* [R] frame-grid slot of a Main or SOLO row, -1 for none */
+  uint64_t seed;             /* Philox key word 0 */
+  int32_t *tokens_out;       /* [R][K]: COND/SOLO sampled, UNCOND = its Main row's,
+                                TEXT: [r][0] greedy text id, the rest pad_id */
+  int32_t *frame_grid;       /* [n_slots][K][F_max] or NULL; cell [slot][k][t - d_k] written */
+  int32_t n_slots, F_max;
+  float *scores;             /* [n_pairs + n_solo][K*V] fp32 in sampled order: the merged,
+                                temperature-divided logits (greedy rows: merged only).
+                                Output of mcd_head_step, input of mcd_sample_step. */
+  void *workspace;
+  size_t workspace_bytes;
+} mcd_step_args;
+
+/* The whole hot path of one step: projection + merge + temperature (scores),
+ * text-head greedy argmax, selection, draw, pads, companion copy, grid scatter.
+ * Two kernel launches on `stream`; no allocation, no synchronisation. */
+mcd_status mcd_head_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
+
+/* Only the sampling part, from caller-provided scores (args->scores, same
+ * layout as above): selection, draw, pads, companion copy and grid scatter for
+ * the audio rows.  TEXT rows are left untouched. */
+mcd_status mcd_sample_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
+
+/* ---- delay pattern (Sec. 2.1) --------------------------------------------
+ * De-interleave at request completion: grid[r][k][f] = streams[r][f + d_k][k]
+ * for f < T - max_k d_k.  streams: [n_req][T][K], grid: [n_req][K][T - max d]. */
+mcd_status mcd_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,
+                            const int32_t *delays /*[host][K]*/, int32_t *grid,
+                            hipStream_t stream);
+/* Inverse: streams[r][t][k] = grid[r][k][t - d_k] where 0 <= t - d_k < F, else
+ * pad_id.  grid: [n_req][K][F], streams: [n_req][F + max d][K]. */
+mcd_status mcd_interleave(const int32_t *grid, int32_t n_req, int32_t F, int32_t K,
+                          const int32_t *delays /*[host][K]*/, int32_t pad_id,
+                          int32_t *streams, hipStream_t stream);
+
+/* Synchronises `stream`, returns the status word in *code and clears it. */
+mcd_status mcd_read_device_status(void *workspace, uint32_t *code, hipStream_t stream);
+
+const char *mcd_status_string(mcd_status s);
+const char *mcd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MCD_H */

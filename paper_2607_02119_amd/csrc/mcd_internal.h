@@ -1,0 +1,75 @@
+// Internal declarations shared by the host API and the gfx950 kernels of libmcd.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mcd.h"
+
+namespace mcd {
+
+// Plan layout (int32 words): header, then the GEMM row order of the audio rows
+// (Main, Companion of pair 0, pair 1, ..., then the solo rows), then the text rows.
+constexpr int32_t kPlanMagic = 0x4D434450;  // "MCDP"
+constexpr int kPlanHeader = 8;
+enum { kPlanMagicWord = 0, kPlanR = 1, kPlanPairs = 2, kPlanSolo = 3, kPlanText = 4 };
+
+constexpr int kStatusBytes = 256;  // status word region at the start of the workspace
+
+// Columns of a text-head tile; the text GEMM writes one (max, argmax) partial per
+// row for every kTextPartCols columns.
+constexpr int kTextPartCols = 64;
+
+struct Delays {
+  int32_t d[MCD_MAX_K];
+};
+
+// Head, by value in kernel arguments.
+struct HeadView {
+  int32_t H, K, V, N, pad_id, V_text;
+  int32_t dtype;
+  const void *W;
+  const float *bias;
+  const void *W_text;
+  Delays delays;
+};
+
+// One step, by value in kernel arguments.
+struct StepView {
+  int32_t R, n_pairs, n_solo, n_text, Mg, Rs;
+  const int32_t *plan;
+  const void *hidden;
+  const float *cfg_w;
+  const float *temperature;
+  const int32_t *top_k;
+  const float *top_p;
+  const uint64_t *rng_key;
+  const int32_t *step;
+  const int32_t *n_frames;
+  const int32_t *grid_slot;
+  uint64_t seed;
+  int32_t *tokens_out;
+  int32_t *frame_grid;
+  int32_t n_slots, F_max;
+  float *scores;
+  uint32_t *status;
+  float *text_val;      // [n_text][text_parts]
+  int32_t *text_idx;    // [n_text][text_parts]
+  int32_t text_parts;
+};
+
+inline int32_t text_parts_for(int32_t V_text) {
+  return (V_text + kTextPartCols - 1) / kTextPartCols;
+}
+
+// Kernel launchers (one .hip file each).
+hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t stream);
+hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
+                         hipStream_t stream);
+hipError_t launch_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,
+                               const Delays &d, int32_t F, int32_t *grid, hipStream_t stream);
+hipError_t launch_interleave(const int32_t *grid, int32_t n_req, int32_t F, int32_t K,
+                             const Delays &d, int32_t T, int32_t pad_id, int32_t *streams,
+                             hipStream_t stream);
+
+}  // namespace mcd

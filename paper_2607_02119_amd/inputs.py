@@ -213,3 +213,14 @@ def make_batch(wl: Workload, t: int, layout: dict | None = None, seed_h: int = S
         step=np.full(R, t, np.int32),
         n_frames=np.full(R, wl.frames, np.int32),
     )
+
+
+def make_scores(Rs: int, N: int, t: int, sigma: float = 1.0, quantum: float = 0.0,
+                seed: int = 77) -> np.ndarray:
+    """Ready-made fp32 scores [Rs][N] for driving the sampling stage on its own:
+    N(0, sigma^2) from default_rng([seed, t]); with quantum > 0, rounded to
+    multiples of it so that exact ties occur."""
+    s = np.random.default_rng([seed, t]).standard_normal((Rs, N)) * sigma
+    if quantum > 0:
+        s = np.round(s / quantum) * quantum
+    return np.ascontiguousarray(s, dtype=np.float32)

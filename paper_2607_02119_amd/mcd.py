@@ -1,0 +1,248 @@
+"""Thin ctypes binding of libmcd (include/mcd.h).
+
+Every function named ``mcd_*`` here marshals its arguments to the C function of
+the same name; all computation happens in the library's HIP kernels.  PyTorch
+supplies device memory and the stream.  ``Head`` is a small convenience wrapper
+that keeps the borrowed weight tensors alive next to the handle.
+
+Importing this module loads ``libmcd.so`` and raises if it has not been built
+(``python -m paper_2607_02119_amd.build``); there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loads the HIP runtime libmcd binds to (same soname, one runtime per process)
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmcd.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2607_02119_amd.build`")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+MCD_OK, MCD_E_INVALID, MCD_E_UNSUPPORTED, MCD_E_WORKSPACE, MCD_E_HIP = range(5)
+MCD_F32, MCD_BF16 = 0, 1
+MCD_ROW_COND, MCD_ROW_UNCOND, MCD_ROW_SOLO, MCD_ROW_TEXT = 0, 1, 2, 3
+MCD_DEV_BAD_PARAM, MCD_DEV_GRID_RANGE, MCD_DEV_BAD_PLAN = 1, 2, 4
+MCD_MAX_K, MCD_MAX_V = 32, 4096
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+
+
+class mcd_head_desc(ctypes.Structure):
+    _fields_ = [("H", _i32), ("K", _i32), ("V", _i32), ("pad_id", _i32),
+                ("delays", _vp), ("dtype", ctypes.c_int), ("W", _vp), ("bias", _vp),
+                ("V_text", _i32), ("W_text", _vp)]
+
+
+class mcd_batch_counts(ctypes.Structure):
+    _fields_ = [("n_pairs", _i32), ("n_solo", _i32), ("n_text", _i32)]
+
+
+class mcd_step_args(ctypes.Structure):
+    _fields_ = [("R", _i32), ("counts", mcd_batch_counts), ("plan", _vp), ("hidden", _vp),
+                ("cfg_w", _vp), ("temperature", _vp), ("top_k", _vp), ("top_p", _vp),
+                ("rng_key", _vp), ("step", _vp), ("n_frames", _vp), ("grid_slot", _vp),
+                ("seed", ctypes.c_uint64), ("tokens_out", _vp), ("frame_grid", _vp),
+                ("n_slots", _i32), ("F_max", _i32), ("scores", _vp), ("workspace", _vp),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+def _sig(name, res, *args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = list(args)
+    return f
+
+
+_mcd_head_create = _sig("mcd_head_create", ctypes.c_int, ctypes.POINTER(mcd_head_desc),
+                        ctypes.POINTER(_vp))
+_mcd_head_destroy = _sig("mcd_head_destroy", None, _vp)
+_mcd_plan_words = _sig("mcd_plan_words", ctypes.c_size_t, _i32)
+_mcd_batch_plan = _sig("mcd_batch_plan", ctypes.c_int, _vp, _i32, _vp, _vp, _vp, ctypes.c_size_t,
+                       ctypes.POINTER(mcd_batch_counts))
+_mcd_plan_sampled_row = _sig("mcd_plan_sampled_row", ctypes.c_int, _vp, _i32,
+                             ctypes.POINTER(_i32), ctypes.POINTER(_i32))
+_mcd_workspace_bytes = _sig("mcd_workspace_bytes", ctypes.c_size_t, _vp, _i32)
+_mcd_head_step = _sig("mcd_head_step", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
+_mcd_sample_step = _sig("mcd_sample_step", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
+_mcd_deinterleave = _sig("mcd_deinterleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _vp, _vp)
+_mcd_interleave = _sig("mcd_interleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _i32, _vp, _vp)
+_mcd_read_device_status = _sig("mcd_read_device_status", ctypes.c_int, _vp,
+                               ctypes.POINTER(ctypes.c_uint32), _vp)
+_mcd_status_string = _sig("mcd_status_string", ctypes.c_char_p, ctypes.c_int)
+_mcd_last_error = _sig("mcd_last_error", ctypes.c_char_p)
+
+EXPORTED = ["mcd_head_create", "mcd_head_destroy", "mcd_plan_words", "mcd_batch_plan",
+            "mcd_plan_sampled_row", "mcd_workspace_bytes", "mcd_head_step", "mcd_sample_step",
+            "mcd_deinterleave", "mcd_interleave", "mcd_read_device_status", "mcd_status_string",
+            "mcd_last_error"]
+
+
+class McdError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        msg = _mcd_last_error().decode(errors="replace")
+        super().__init__(f"{where}: {mcd_status_string(code)} ({msg})")
+
+
+def _check(code, where):
+    if code != MCD_OK:
+        raise McdError(code, where)
+
+
+def _ptr(t):
+    """Device (or host numpy) pointer of an optional tensor / array."""
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        return t.data_ptr()
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return int(t)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if isinstance(stream, torch.cuda.Stream) else int(stream)
+
+
+# ---------------------------------------------------------------------------
+# C functions, one to one
+
+def mcd_status_string(code):
+    return _mcd_status_string(code).decode()
+
+
+def mcd_last_error():
+    return _mcd_last_error().decode(errors="replace")
+
+
+def mcd_head_create(H, K, V, pad_id, delays, dtype, W, bias=None, V_text=0, W_text=None):
+    d = np.ascontiguousarray(delays, dtype=np.int32)
+    desc = mcd_head_desc(H, K, V, pad_id, d.ctypes.data, dtype, _ptr(W), _ptr(bias), V_text,
+                         _ptr(W_text))
+    h = _vp()
+    _check(_mcd_head_create(ctypes.byref(desc), ctypes.byref(h)), "mcd_head_create")
+    return h
+
+
+def mcd_head_destroy(h):
+    _mcd_head_destroy(h)
+
+
+def mcd_plan_words(R):
+    return int(_mcd_plan_words(R))
+
+
+def mcd_batch_plan(h, pair_map, row_kind):
+    """Host plan of a batch -> (plan int32 numpy array, mcd_batch_counts)."""
+    pm = np.ascontiguousarray(pair_map, dtype=np.int32)
+    rk = np.ascontiguousarray(row_kind, dtype=np.uint8)
+    R = pm.shape[0]
+    plan = np.zeros(mcd_plan_words(R), dtype=np.int32)
+    counts = mcd_batch_counts()
+    _check(_mcd_batch_plan(h, R, pm.ctypes.data, rk.ctypes.data, plan.ctypes.data, plan.shape[0],
+                           ctypes.byref(counts)), "mcd_batch_plan")
+    return plan, counts
+
+
+def mcd_plan_sampled_row(plan, s):
+    row, comp = _i32(), _i32()
+    _check(_mcd_plan_sampled_row(plan.ctypes.data, s, ctypes.byref(row), ctypes.byref(comp)),
+           "mcd_plan_sampled_row")
+    return row.value, comp.value
+
+
+def mcd_workspace_bytes(h, R):
+    return int(_mcd_workspace_bytes(h, R))
+
+
+def _step_args(R, counts, plan, hidden, cfg_w, temperature, top_k, top_p, rng_key, step,
+               n_frames, grid_slot, seed, tokens_out, frame_grid, n_slots, F_max, scores,
+               workspace):
+    return mcd_step_args(R, counts, _ptr(plan), _ptr(hidden), _ptr(cfg_w), _ptr(temperature),
+                         _ptr(top_k), _ptr(top_p), _ptr(rng_key), _ptr(step), _ptr(n_frames),
+                         _ptr(grid_slot), seed, _ptr(tokens_out), _ptr(frame_grid), n_slots,
+                         F_max, _ptr(scores), _ptr(workspace),
+                         0 if workspace is None else workspace.numel() * workspace.element_size())
+
+
+def mcd_head_step(h, stream=None, **kw):
+    a = _step_args(**kw)
+    _check(_mcd_head_step(h, ctypes.byref(a), _stream(stream)), "mcd_head_step")
+
+
+def mcd_sample_step(h, stream=None, **kw):
+    a = _step_args(**kw)
+    _check(_mcd_sample_step(h, ctypes.byref(a), _stream(stream)), "mcd_sample_step")
+
+
+def mcd_deinterleave(streams, delays, grid, stream=None):
+    """streams: int32 [n_req][T][K] -> grid int32 [n_req][K][T - max d] (device tensors)."""
+    n_req, T, K = streams.shape
+    d = np.ascontiguousarray(delays, dtype=np.int32)
+    _check(_mcd_deinterleave(_ptr(streams), n_req, T, K, d.ctypes.data, _ptr(grid),
+                             _stream(stream)), "mcd_deinterleave")
+
+
+def mcd_interleave(grid, delays, pad_id, streams, stream=None):
+    """grid: int32 [n_req][K][F] -> streams int32 [n_req][F + max d][K] (device tensors)."""
+    n_req, K, F = grid.shape
+    d = np.ascontiguousarray(delays, dtype=np.int32)
+    _check(_mcd_interleave(_ptr(grid), n_req, F, K, d.ctypes.data, pad_id, _ptr(streams),
+                           _stream(stream)), "mcd_interleave")
+
+
+def mcd_read_device_status(workspace, stream=None):
+    code = ctypes.c_uint32()
+    _check(_mcd_read_device_status(_ptr(workspace), ctypes.byref(code), _stream(stream)),
+           "mcd_read_device_status")
+    return code.value
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrapper
+
+class Head:
+    """Handle plus the device tensors it borrows."""
+
+    def __init__(self, W, delays, pad_id, bias=None, W_text=None):
+        assert W.is_cuda and W.dim() == 3 and W.is_contiguous()
+        K, V, H = W.shape
+        dtype = {torch.bfloat16: MCD_BF16, torch.float32: MCD_F32}[W.dtype]
+        self.W, self.bias, self.W_text = W, bias, W_text
+        self.H, self.K, self.V, self.pad_id = H, K, V, int(pad_id)
+        self.delays = np.ascontiguousarray(delays, dtype=np.int32)
+        self.V_text = 0 if W_text is None else W_text.shape[0]
+        self.handle = mcd_head_create(H, K, V, self.pad_id, self.delays, dtype, W, bias,
+                                      self.V_text, W_text)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None:
+            mcd_head_destroy(h)
+            self.handle = None
+
+    def plan(self, pair_map, row_kind, device="cuda"):
+        plan, counts = mcd_batch_plan(self.handle, pair_map, row_kind)
+        return Plan(plan, counts, torch.from_numpy(plan).to(device))
+
+    def workspace(self, R, device="cuda"):
+        return torch.zeros(max(mcd_workspace_bytes(self.handle, R), 256), dtype=torch.uint8,
+                           device=device)
+
+
+class Plan:
+    def __init__(self, host, counts, dev):
+        self.host, self.counts, self.dev = host, counts, dev
+        self.R = int(host[1])
+        self.n_pairs, self.n_solo, self.n_text = counts.n_pairs, counts.n_solo, counts.n_text
+        self.Rs = self.n_pairs + self.n_solo
+
+    def sampled_rows(self):
+        """(row, companion) of each sampled index."""
+        return [mcd_plan_sampled_row(self.host, s) for s in range(self.Rs)]

@@ -1,0 +1,88 @@
+"""Comparison helpers for the GPU parity tests (test code: may use the oracle)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+
+EXEMPT = oracle.FLAG_GAP_SMALL | oracle.FLAG_TOPP_EDGE | oracle.FLAG_TOPK_EDGE
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def subset_batch(batch: dict, rows) -> dict:
+    """Sub-batch of the given physical rows (partners must be included)."""
+    rows = np.asarray(rows)
+    inv = {int(r): i for i, r in enumerate(rows)}
+    sub = {}
+    for k, v in batch.items():
+        sub[k] = v[rows] if isinstance(v, np.ndarray) and v.shape[:1] == batch["pair_map"].shape else v
+    sub["pair_map"] = np.array([inv[int(p)] if p >= 0 else -1 for p in batch["pair_map"][rows]],
+                               np.int32)
+    return sub
+
+
+def pick_rows(layout: dict, n_pairs=2, n_solo=2, n_text=2, seed=0):
+    """A few Main rows with their Companions, solo rows and text rows."""
+    rng = np.random.default_rng(seed)
+    kind, pm = layout["row_kind"], layout["pair_map"]
+    out = []
+    conds = np.where(kind == oracle.ROW_COND)[0]
+    for c in rng.choice(conds, min(n_pairs, len(conds)), replace=False) if len(conds) else []:
+        out += [int(c), int(pm[c])]
+    for kd, n in ((oracle.ROW_SOLO, n_solo), (oracle.ROW_TEXT, n_text)):
+        cand = np.where(kind == kd)[0]
+        if len(cand):
+            out += [int(x) for x in rng.choice(cand, min(n, len(cand)), replace=False)]
+    return sorted(out)
+
+
+def score_rel_err(gpu_scores, plan_rows, ora_scores, K, V):
+    """max over (row, k) vectors of max|g - o| / max|o|; plan_rows[s] = physical row."""
+    worst = 0.0
+    for s, r in enumerate(plan_rows):
+        if r is None:
+            continue
+        g = gpu_scores[s].astype(np.float64).reshape(K, V)
+        o = ora_scores[r].reshape(K, V)
+        den = np.maximum(np.abs(o).max(axis=1), 1e-300)
+        worst = max(worst, float((np.abs(g - o).max(axis=1) / den).max()))
+    return worst
+
+
+class TokenCheck:
+    """Accumulates token comparisons with the exemption classes of the oracle."""
+
+    def __init__(self):
+        self.n = 0
+        self.mismatch = 0
+        self.exempt = {"gap": 0, "topp": 0, "topk": 0}
+        self.bad = []
+
+    def add(self, gpu_tok, ora_tok, flags, rows=None, where=""):
+        rows = range(gpu_tok.shape[0]) if rows is None else rows
+        for r in rows:
+            for k in range(gpu_tok.shape[1]):
+                self.n += 1
+                g, o, f = int(gpu_tok[r, k]), int(ora_tok[r, k]), int(flags[r, k])
+                if g == o:
+                    continue
+                self.mismatch += 1
+                if f & oracle.FLAG_GAP_SMALL:
+                    self.exempt["gap"] += 1
+                elif f & oracle.FLAG_TOPP_EDGE:
+                    self.exempt["topp"] += 1
+                elif f & oracle.FLAG_TOPK_EDGE:
+                    self.exempt["topk"] += 1
+                else:
+                    self.bad.append((where, r, k, g, o, f))
+
+    def assert_ok(self, label=""):
+        say(f"[{label}] positions={self.n} mismatches={self.mismatch} exempt={self.exempt} "
+            f"unexplained={len(self.bad)}")
+        assert not self.bad, f"unexplained token mismatches: {self.bad[:10]}"

@@ -1,0 +1,116 @@
+"""Host-side checks of the C ABI (no GPU needed, no kernel launched): the library
+loads, exports every function include/mcd.h declares, and rejects bad
+arguments and inconsistent batches before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mcd.h")
+
+mcd = pytest.importorskip("paper_2607_02119_amd.mcd", reason="libmcd.so not built")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mcd_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    lib = ctypes.CDLL(mcd._LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in mcd.h but not exported"
+    assert sorted(mcd.EXPORTED) == names
+
+
+FAKE_W = 0x10000   # never dereferenced: host-only calls
+
+
+def _head(**kw):
+    args = dict(H=64, K=3, V=50, pad_id=50, delays=[0, 1, 2], dtype=mcd.MCD_BF16, W=FAKE_W)
+    args.update(kw)
+    return mcd.mcd_head_create(**args)
+
+
+def test_head_create_validation():
+    h = _head()
+    mcd.mcd_head_destroy(h)
+    bad = [dict(H=65), dict(K=0, delays=[]), dict(K=33, delays=list(range(33))), dict(V=0),
+           dict(V=mcd.MCD_MAX_V + 1), dict(delays=[0, -1, 2]), dict(W=0), dict(W=FAKE_W + 2),
+           dict(dtype=7), dict(V_text=10, W_text=None)]
+    for b in bad:
+        with pytest.raises(mcd.McdError):
+            _head(**b)
+    h = _head(dtype=mcd.MCD_F32, H=40)
+    mcd.mcd_head_destroy(h)
+
+
+def test_batch_plan_layout_and_errors():
+    h = _head(V_text=100, W_text=FAKE_W)
+    # rows: 0 solo, 1 uncond(->3), 2 text, 3 cond(->1), 4 cond(->5), 5 uncond(->4)
+    pm = [-1, 3, -1, 1, 5, 4]
+    rk = [2, 1, 3, 0, 0, 1]
+    plan, c = mcd.mcd_batch_plan(h, pm, rk)
+    assert (c.n_pairs, c.n_solo, c.n_text) == (2, 1, 1)
+    assert plan[1] == 6 and list(plan[2:5]) == [2, 1, 1]
+    assert list(plan[8:]) == [3, 1, 4, 5, 0, 2]
+    assert mcd.mcd_plan_sampled_row(plan, 0) == (3, 1)
+    assert mcd.mcd_plan_sampled_row(plan, 1) == (4, 5)
+    assert mcd.mcd_plan_sampled_row(plan, 2) == (0, -1)
+    with pytest.raises(mcd.McdError):
+        mcd.mcd_plan_sampled_row(plan, 3)
+    for pm_bad, rk_bad in [([1, 0], [0, 0]),           # partner of the wrong kind
+                           ([1, 2, 1], [0, 1, 1]),     # partner points elsewhere
+                           ([0], [0]),                 # self partner
+                           ([5, 0], [0, 1]),           # out of range
+                           ([0, -1], [2, 2]),          # solo row with a partner
+                           ([-1], [9])]:               # unknown kind
+        with pytest.raises(mcd.McdError):
+            mcd.mcd_batch_plan(h, pm_bad, rk_bad)
+    h2 = _head()
+    with pytest.raises(mcd.McdError):
+        mcd.mcd_batch_plan(h2, [-1], [3])              # text row, no text head
+    assert mcd.mcd_workspace_bytes(h2, 100) == 256
+    assert mcd.mcd_workspace_bytes(h, 4) > 256
+
+
+def test_step_argument_errors_before_launch():
+    h = _head()
+    plan, c = mcd.mcd_batch_plan(h, [1, 0], [0, 1])
+    base = dict(R=2, counts=c, plan=FAKE_W, hidden=FAKE_W, cfg_w=FAKE_W, temperature=FAKE_W,
+                top_k=FAKE_W, top_p=FAKE_W, rng_key=None, step=FAKE_W, n_frames=FAKE_W,
+                grid_slot=FAKE_W, seed=0, tokens_out=FAKE_W, frame_grid=None, n_slots=0, F_max=0,
+                scores=FAKE_W, workspace=None)
+    with pytest.raises(mcd.McdError) as e:
+        mcd.mcd_head_step(h, stream=0, **base)                 # no workspace
+    assert e.value.code == mcd.MCD_E_WORKSPACE
+    for field, val in [("scores", None), ("hidden", None), ("temperature", None),
+                       ("tokens_out", None), ("plan", None), ("R", 3), ("n_slots", -1)]:
+        kw = dict(base, **{field: val})
+        kw["workspace"] = None
+        with pytest.raises(mcd.McdError) as e:
+            mcd.mcd_head_step(h, stream=0, **kw)
+        assert e.value.code in (mcd.MCD_E_INVALID, mcd.MCD_E_WORKSPACE)
+    # misaligned hidden for bf16
+    a = mcd._step_args(**dict(base, hidden=FAKE_W + 2))
+    a.workspace, a.workspace_bytes = 0x100000, 4096
+    rc = mcd._mcd_head_step(h, ctypes.byref(a), None)
+    assert rc == mcd.MCD_E_INVALID and "aligned" in mcd.mcd_last_error()
+
+
+def test_interleave_argument_errors():
+    with pytest.raises(mcd.McdError):
+        mcd._check(mcd._mcd_deinterleave(FAKE_W, 1, 2, 3, np.array([0, 1, 5], np.int32).ctypes.data,
+                                         FAKE_W, None), "x")      # T shorter than a delay
+    with pytest.raises(mcd.McdError):
+        mcd._check(mcd._mcd_interleave(FAKE_W, 1, 4, 0, None, 0, FAKE_W, None), "x")
+    # empty work is a no-op, not an error
+    mcd._check(mcd._mcd_deinterleave(None, 0, 5, 2, np.array([0, 1], np.int32).ctypes.data,
+                                     None, None), "x")
+    assert mcd.mcd_status_string(mcd.MCD_E_HIP) == "hip error"

@@ -1,0 +1,292 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Tolerances:
+  * merged, temperature-divided scores: max over (row, codebook) vectors of
+    max|gpu - oracle| / max|oracle| <= 1e-5 for fp32 inputs, 1e-2 for bf16;
+  * tokens and frame grids: bit-exact, except at positions the oracle flags as
+    ambiguous: top-2 perturbed (or greedy) gap below GAP_TOL, or a top-k / top-p
+    boundary within TOPK_TOL / TOPP_TOL.  Those are counted and printed.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_02119_amd import inputs
+from tests._compare import TokenCheck, pick_rows, say, score_rel_err, subset_batch
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2607_02119_amd import harness, mcd  # noqa: E402
+
+GAP_TOL = 1e-3
+# End to end the GPU scores carry fp32 accumulation error (about 1e-6 relative
+# for H = 4096); a top-k or top-p cut whose deciding margin is below these
+# bounds can flip legitimately.
+TOPK_TOL = 1e-4
+TOPP_TOL = 1e-5
+
+
+def _cpu(t):
+    return t.detach().cpu().numpy()
+
+
+def _oracle_step(dw, t, rows=None):
+    b = inputs.make_batch(dw.wl, t, dw.layout)
+    if rows is not None:
+        b = subset_batch(b, rows)
+    return b, oracle.head_step(dw.host_head, b, seed=dw.seed, gap_tol=GAP_TOL, topk_tol=TOPK_TOL,
+                               topp_tol=TOPP_TOL)
+
+
+def _plan_rows(dw, rows=None):
+    """Physical row (or its index in `rows`) of every sampled index."""
+    out = []
+    pos = None if rows is None else {r: i for i, r in enumerate(rows)}
+    for r, _ in dw.plan.sampled_rows():
+        out.append(r if pos is None else pos.get(r))
+    return out
+
+
+def _check_step(dw, t, tc, rows=None, score_tol=None):
+    """Run step t on the GPU (whole batch), the oracle on `rows` (default all)."""
+    dw.tokens.fill_(-1)
+    dw.run_step(t, hidden_index=dw.hidden_steps.index(t))
+    torch.cuda.synchronize()
+    g_tok, g_sc = _cpu(dw.tokens), _cpu(dw.scores)
+    b, o = _oracle_step(dw, t, rows)
+    sel = np.arange(dw.wl.R) if rows is None else np.asarray(rows)
+    tc.add(g_tok[sel], o["tokens"], o["flags"], where=f"t={t}")
+    if score_tol is not None and dw.wl.Rs:
+        err = score_rel_err(g_sc, _plan_rows(dw, None if rows is None else list(sel)), o["scores"],
+                            dw.wl.K, dw.wl.V)
+        say(f"  t={t} score rel err {err:.3e}")
+        assert err <= score_tol
+    return g_tok, o
+
+
+# ---------------------------------------------------------------------------
+def test_tiny_ref_full_run_tokens_scores_grid():
+    """The fp32 tiny reference workload, all 32 steps, every row."""
+    wl = inputs.WORKLOADS["tiny_ref"]
+    say(f"case tiny_ref R={wl.R} H={wl.H} K={wl.K} V={wl.V}")
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    tc = TokenCheck()
+    ora_grid = np.full((wl.n_slots, wl.K, wl.frames), -1, np.int32)
+    for t in range(wl.steps):
+        b, o = _oracle_step(dw, t)
+        oracle.head_step(dw.host_head, b, seed=0, n_slots=wl.n_slots, F_max=wl.frames,
+                         frame_grid=ora_grid, want_scores=False)
+        _check_step(dw, t, tc, score_tol=1e-5)
+    tc.assert_ok("tiny_ref")
+    assert tc.mismatch == 0
+    g = _cpu(dw.grid)
+    assert (ora_grid >= 0).all()
+    assert np.array_equal(g, ora_grid)
+    assert dw.status() == 0
+
+
+RAGGED = [
+    # name, workload kwargs
+    ("bf16_ragged_mixed", dict(H=128, K=3, V=37, n_pairs=70, n_solo=5, n_text=3, V_text=300,
+                               dtype="bf16", top_k=7, temperature=0.7, steps=6, shuffle=True)),
+    ("bf16_topp_two_tiles", dict(H=192, K=2, V=333, n_pairs=20, n_solo=3, dtype="bf16",
+                                 top_p=0.9, cfg_w=2.0, steps=4)),
+    ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
+                              dtype="f32", top_k=5, top_p=0.8, steps=5, shuffle=True)),
+    ("bf16_greedy", dict(H=64, K=4, V=100, n_pairs=5, n_solo=4, dtype="bf16", temperature=0.0,
+                         steps=6)),
+    ("bf16_single_row", dict(H=64, K=1, V=1, n_pairs=0, n_solo=1, dtype="bf16", steps=2)),
+    ("bf16_only_text", dict(H=64, K=2, V=16, n_pairs=0, n_solo=0, n_text=5, V_text=129,
+                            dtype="bf16", steps=2)),
+]
+
+
+@pytest.mark.parametrize("name,kw", RAGGED, ids=[r[0] for r in RAGGED])
+def test_ragged_shapes_every_step(name, kw):
+    wl = inputs.Workload(name, **kw)
+    say(f"case {name} R={wl.R} Mg={2 * wl.n_pairs + wl.n_solo} N={wl.N} text={wl.n_text}")
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    tc = TokenCheck()
+    tol = 1e-5 if wl.dtype == "f32" else 1e-2
+    for t in range(wl.steps):
+        _check_step(dw, t, tc, score_tol=tol)
+    tc.assert_ok(name)
+    assert dw.status() == 0
+
+
+SAMPLER = [
+    # V, K, Rs, sigma, quantum, temperature, top_k, top_p
+    (2048, 8, 16, 3.6, 0.0, 0.9, 50, 1.0),
+    (4096, 8, 8, 2.24, 0.0, 1.0, 0, 0.95),
+    (1024, 16, 16, 3.6, 0.0, 0.8, 20, 1.0),
+    (4096, 2, 4, 1.0, 0.25, 1.0, 50, 0.9),      # heavy ties at both boundaries
+    (37, 3, 5, 1.0, 0.5, 1.0, 5, 0.7),
+    (1000, 2, 3, 0.0, 0.0, 1.0, 10, 0.5),        # all scores equal
+    (4096, 1, 4, 2.0, 0.0, 0.0, 0, 1.0),         # greedy
+    (4096, 2, 4, 2.0, 0.0, 1.0, 1, 1.0),         # top-k = 1
+    (512, 2, 4, 2.0, 0.0, 1.0, 0, 1e-6),         # tiny p: argmax
+    (512, 2, 4, 2.0, 0.0, 1.0, 0, 0.999999),     # p near one
+]
+
+
+@pytest.mark.parametrize("V,K,Rs,sigma,quantum,T,top_k,top_p", SAMPLER)
+def test_sampler_alone_matches_oracle_exactly(V, K, Rs, sigma, quantum, T, top_k, top_p):
+    """Selection + draw fed the same fp32 scores on both sides: tokens must agree
+    bit for bit (tolerances only for gaps below 1e-9)."""
+    wl = inputs.Workload("sampler", H=64, K=K, V=V, n_pairs=0, n_solo=Rs, temperature=T,
+                         top_k=top_k, top_p=top_p, steps=K + 3)
+    say(f"case sampler V={V} K={K} Rs={Rs} T={T} top_k={top_k} top_p={top_p} q={quantum}")
+    dw = harness.DeviceWorkload(wl, weights=dict(H=64, K=K, V=V, pad_id=V,
+                                                 delays=np.arange(K, dtype=np.int32),
+                                                 W=np.zeros((K, V, 64), np.uint16), bias=None,
+                                                 W_text=None))
+    tc = TokenCheck()
+    for t in range(wl.steps):
+        sc = inputs.make_scores(Rs, wl.N, t, sigma=sigma, quantum=quantum)
+        dw.tokens.fill_(-1)
+        dw.sample_only(t, harness.to_device(sc))
+        torch.cuda.synchronize()
+        g = _cpu(dw.tokens)
+        b = inputs.make_batch(wl, t, dw.layout)
+        srow = [r for r, _ in dw.plan.sampled_rows()]
+        o = oracle.sample_rows(dw.host_head, b, srow, [-1] * Rs, sc.astype(np.float64),
+                               gap_tol=1e-9, topk_tol=0.0, topp_tol=1e-9)
+        tc.add(g, o["tokens"], o["flags"], where=f"t={t}")
+    tc.assert_ok("sampler")
+    assert tc.mismatch == 0
+
+
+def test_interleave_roundtrip_on_device():
+    rng = np.random.default_rng(0)
+    for n_req, K, F, dmax in [(3, 4, 29, 3), (5, 8, 249, 7), (2, 3, 0, 2), (4, 5, 17, 9)]:
+        delays = np.sort(rng.integers(0, dmax + 1, K)).astype(np.int32)
+        delays[-1] = dmax
+        G = rng.integers(0, 1024, (n_req, K, F)).astype(np.int32)
+        T = F + dmax
+        say(f"case interleave n_req={n_req} K={K} F={F} delays={delays.tolist()}")
+        gd = torch.from_numpy(G).cuda()
+        sd = torch.full((n_req, T, K), -7, dtype=torch.int32, device="cuda")
+        mcd.mcd_interleave(gd, delays, 1024, sd)
+        back = torch.full_like(gd, -7)
+        mcd.mcd_deinterleave(sd, delays, back)
+        torch.cuda.synchronize()
+        S = _cpu(sd)
+        for r in range(n_req):
+            assert np.array_equal(S[r], oracle.interleave(G[r], delays, 1024))
+        assert np.array_equal(_cpu(back), G)
+
+
+def test_per_step_scatter_equals_completion_deinterleave():
+    """The grid written step by step equals the de-interleave of the emitted streams."""
+    wl = inputs.Workload("scatter", H=64, K=4, V=64, n_pairs=3, n_solo=2, top_k=8, steps=11)
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    streams = np.zeros((wl.n_slots, wl.steps, wl.K), np.int32)
+    for t in range(wl.steps):
+        dw.run_step(t)
+        torch.cuda.synchronize()
+        tok = _cpu(dw.tokens)
+        for r in range(wl.R):
+            slot = dw.layout["grid_slot"][r]
+            if slot >= 0:
+                streams[slot, t] = tok[r]
+    grid = torch.full((wl.n_slots, wl.K, wl.frames), -1, dtype=torch.int32, device="cuda")
+    mcd.mcd_deinterleave(torch.from_numpy(streams).cuda(), dw.host_head["delays"], grid)
+    torch.cuda.synchronize()
+    assert np.array_equal(_cpu(grid), _cpu(dw.grid))
+    # pads: K(K-1) per request over the full run
+    assert ((streams == wl.pad).sum(axis=(1, 2)) == wl.K * (wl.K - 1)).all()
+
+
+def test_companion_copy_and_determinism():
+    wl = inputs.Workload("det", H=128, K=4, V=256, n_pairs=8, n_solo=3, top_k=20, steps=6,
+                         shuffle=True)
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    runs = []
+    for _ in range(2):
+        dw.grid.fill_(-1)
+        toks = []
+        for t in range(wl.steps):
+            dw.run_step(t)
+            torch.cuda.synchronize()
+            toks.append(_cpu(dw.tokens).copy())
+            if _ == 0:
+                tok = toks[-1]
+                for r in np.where(dw.layout["row_kind"] == inputs.ROW_UNCOND)[0]:
+                    assert np.array_equal(tok[r], tok[dw.layout["pair_map"][r]])
+        runs.append((np.stack(toks), _cpu(dw.grid).copy(), _cpu(dw.scores).copy()))
+    assert np.array_equal(runs[0][0], runs[1][0])
+    assert np.array_equal(runs[0][1], runs[1][1])
+    assert np.array_equal(runs[0][2].view(np.uint32), runs[1][2].view(np.uint32))
+
+
+def test_cfg_w0_w1_against_solo_logits_on_gpu():
+    """Eq. 1 on the GPU: w = 1 reproduces the Main row's own logits and w = 0 the
+    Companion's, bit for bit, as computed by the same kernel for a solo row."""
+    H, K, V = 128, 2, 160
+    wl_pair = inputs.Workload("w", H=H, K=K, V=V, n_pairs=1, temperature=1.0, steps=2)
+    wl_solo = inputs.Workload("s", H=H, K=K, V=V, n_pairs=0, n_solo=2, temperature=1.0, steps=2)
+    head = inputs.make_weights(wl_pair)
+    dp = harness.DeviceWorkload(wl_pair, weights=head)
+    ds = harness.DeviceWorkload(wl_solo, weights=head)
+    hid = harness.to_device(inputs.make_hidden(wl_pair, 0))
+    ds.hidden = hid[None]
+    ds.run_step(0, hidden_index=0)
+    torch.cuda.synchronize()
+    solo = _cpu(ds.scores)
+    dp.hidden = hid[None]
+    for w, want in ((1.0, solo[0]), (0.0, solo[1])):
+        dp.params["cfg_w"].fill_(w)
+        dp.run_step(0, hidden_index=0)
+        torch.cuda.synchronize()
+        assert np.array_equal(_cpu(dp.scores)[0].view(np.uint32), want.view(np.uint32))
+
+
+def test_device_status_bad_parameter_pads_and_flags():
+    wl = inputs.Workload("bad", H=64, K=2, V=32, n_pairs=1, n_solo=1, top_k=4, steps=3)
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    dw.params["temperature"][2] = -1.0    # the solo row
+    dw.run_step(2)
+    torch.cuda.synchronize()
+    assert dw.status() == mcd.MCD_DEV_BAD_PARAM
+    assert dw.status() == 0                # read clears it
+    assert (_cpu(dw.tokens)[2] == wl.pad).all()
+
+
+# ---------------------------------------------------------------------------
+# Benchmark-sized workloads: GPU on the whole batch, the oracle on sampled rows.
+
+FULL = [("memory_bound_decode", [7, 130, 253]), ("weight_streaming", [7, 300, 511]),
+        ("mfma_mixed", [7, 125]), ("cfg_on", [15, 250]), ("cfg_off", [15])]
+
+
+@pytest.mark.parametrize("name,steps", FULL, ids=[f[0] for f in FULL])
+def test_full_size_sampled_rows(name, steps):
+    wl = inputs.WORKLOADS[name]
+    say(f"case full-size {name} R={wl.R} H={wl.H} N={wl.N} text={wl.n_text} steps={steps}")
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden(steps)
+    rows = pick_rows(dw.layout, n_pairs=2, n_solo=2, n_text=1)
+    tc = TokenCheck()
+    for t in steps:
+        g_tok, o = _check_step(dw, t, tc, rows=rows, score_tol=1e-2)
+        # the grid cells of this step for the sampled rows
+        grid = _cpu(dw.grid)
+        for i, r in enumerate(rows):
+            slot = dw.layout["grid_slot"][r]
+            if slot < 0:
+                continue
+            for k in range(wl.K):
+                f = t - dw.host_head["delays"][k]
+                if 0 <= f < wl.frames:
+                    assert grid[slot, k, f] == g_tok[r, k]
+    tc.assert_ok(name)
+    assert dw.status() == 0
