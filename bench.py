@@ -1,0 +1,201 @@
+"""Throughput of the multi-codebook decode head on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--weight-copies C]
+
+A step is one pass of the whole hot path (mcd_head_step: head projections with
+the fused CFG merge and temperature, text-head argmax, selection, Gumbel-max
+draw, pads, companion copy, frame-grid scatter) over one batch of the workload.
+Inputs are resident in HBM before timing; the timed loop walks the workload's
+decode steps (each with its own hidden states and step index) and rotates
+through several copies of the weights so that they stream from HBM rather than
+from the 256 MB Infinity Cache.
+
+Prints one JSON line: value = client-visible codebook tokens per second
+(sampled rows x codebooks per step / step time), the roofline of the head
+projection kernel (the dominant one), and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector
+MALL_BYTES = 256 * 2**20       # Infinity Cache
+
+
+def algorithmic(wl):
+    """Bytes and flops the head projection must move / do per step (one launch)."""
+    eb = wl.elem_bytes()
+    Mg = 2 * wl.n_pairs + wl.n_solo
+    w_bytes = wl.N * wl.H * eb + wl.V_text * wl.H * eb
+    hid = wl.R * wl.H * eb
+    flops = 2.0 * Mg * wl.N * wl.H + 2.0 * wl.n_text * wl.V_text * wl.H
+    return dict(weight_bytes=w_bytes, hidden_bytes=hid, bytes=w_bytes + hid, flops=flops,
+                scores_bytes=4 * wl.Rs * wl.N)
+
+
+def cpu_baseline(wl, budget_s=15.0):
+    """The CPU oracle (single-threaded, fp64) on a bounded sample of the workload:
+    whole Main/Companion pairs (or solo rows) of one decode step, added until
+    about budget_s seconds of CPU work.  Returns codebook tokens per second."""
+    import oracle
+    from paper_2607_02119_amd import inputs
+
+    t = wl.K + 1
+    lay = inputs.row_layout(wl)
+    head = inputs.make_weights(wl)
+    b = inputs.make_batch(wl, t, lay)
+    kinds = lay["row_kind"]
+    units = []   # lists of physical rows forming one sampled request
+    for r in range(wl.R):
+        if kinds[r] == inputs.ROW_COND:
+            units.append([r, int(lay["pair_map"][r])])
+        elif kinds[r] == inputs.ROW_SOLO:
+            units.append([r])
+    done_rows, tokens, elapsed = [], 0, 0.0
+    for u in units:
+        rows = u
+        inv = {x: i for i, x in enumerate(rows)}
+        sub = {k: (v[rows] if isinstance(v, np.ndarray) and v.shape[:1] == (wl.R,) else v)
+               for k, v in b.items()}
+        sub["pair_map"] = np.array([inv[p] if p >= 0 else -1 for p in b["pair_map"][rows]],
+                                   np.int32)
+        t0 = time.perf_counter()
+        oracle.head_step(head, sub, seed=0, want_scores=False)
+        elapsed += time.perf_counter() - t0
+        tokens += wl.K
+        done_rows += rows
+        if elapsed >= budget_s:
+            break
+    return dict(value=tokens / elapsed, unit="codebook tokens/s", cores=1, kind="oracle",
+                sample=f"decode step {t}: {len(done_rows)} of {wl.R} rows "
+                       f"({tokens} codebook tokens), {elapsed:.1f} s single-threaded fp64")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", default="weight_streaming")
+    ap.add_argument("--weight-copies", type=int, default=0,
+                    help="weight copies rotated per step (0: enough to exceed 3x the MALL)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the head stage is single-GPU in this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_02119_amd import harness, inputs
+
+    wl = inputs.WORKLOADS[args.workload]
+    alg = algorithmic(wl)
+    copies = args.weight_copies or max(1, math.ceil(3 * MALL_BYTES / alg["weight_bytes"]))
+    torch.cuda.set_device(0)
+    dw = harness.DeviceWorkload(wl, weight_copies=copies)
+    n_hidden = min(wl.steps, args.steps + args.warmup)
+    dw.load_hidden(range(n_hidden))
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        t = i % n_hidden
+        dw.run_step(t, hidden_index=t, copy=i % copies, stream=stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    status = dw.status()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    status |= dw.status()
+
+    # per-launch durations of the two kernels, events around each launch
+    def per_launch(fn):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i, (a, b) in enumerate(evs):
+            a.record(stream)
+            fn(args.warmup + i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+
+    def logits(i):
+        t = i % n_hidden
+        dw.run_logits(t, hidden_index=t, copy=i % copies, stream=stream)
+
+    def sample(i):
+        dw.run_sample(i % n_hidden, copy=i % copies, stream=stream)
+
+    ms_k1 = per_launch(logits)
+    ms_k2 = per_launch(sample)
+    status |= dw.status()
+
+    tokens_per_step = wl.Rs * wl.K
+    value = tokens_per_step / (ms_step * 1e-3)
+    mfma_bound = alg["flops"] / (BF16_PEAK_TFLOPS * 1e12) > alg["bytes"] / (HBM_PEAK_GBS * 1e9)
+    if mfma_bound:
+        ach = alg["flops"] / (ms_k1 * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                    frac=round(ach / BF16_PEAK_TFLOPS, 4))
+    else:
+        ach = alg["bytes"] / (ms_k1 * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(ach / HBM_PEAK_GBS, 4))
+    roof.update(traffic=None, kernel="head_gemm (mcd_head_logits)",
+                us_per_launch=round(ms_k1 * 1e3, 2),
+                algorithmic_bytes=alg["bytes"], algorithmic_flops=alg["flops"])
+    out = {
+        "metric": "codebook tokens/sec per CFG-paired decode step",
+        "value": round(value, 1),
+        "unit": "codebook tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded; shapes of the workload table)",
+        "config": {"workload": wl.name, "rows": wl.R, "cfg_pairs": wl.n_pairs,
+                   "solo_rows": wl.n_solo, "text_rows": wl.n_text, "H": wl.H, "K": wl.K,
+                   "V": wl.V, "V_text": wl.V_text, "cfg_w": wl.cfg_w,
+                   "temperature": wl.temperature, "top_k": wl.top_k, "top_p": wl.top_p,
+                   "weight_copies": copies, "parallelism": "single GPU"},
+        "roofline": roof,
+        "step": {"hbm_frac": round(alg["bytes"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "mfma_frac": round(alg["flops"] / (ms_step * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                 "us_sample_kernel": round(ms_k2 * 1e3, 2),
+                 "device_status": status},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

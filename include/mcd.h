@@ -147,12 +147,23 @@ typedef struct {
 
 /* The whole hot path of one step: projection + merge + temperature (scores),
  * text-head greedy argmax, selection, draw, pads, companion copy, grid scatter.
- * Two kernel launches on `stream`; no allocation, no synchronisation. */
+ * Equal to mcd_head_logits followed by mcd_sample_step: two kernel launches on
+ * `stream`; no allocation, no synchronisation. */
 mcd_status mcd_head_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
 
-/* Only the sampling part, from caller-provided scores (args->scores, same
- * layout as above): selection, draw, pads, companion copy and grid scatter for
- * the audio rows.  TEXT rows are left untouched. */
+/* First half of a step: the K head projections of every audio row with the
+ * CFG merge (Eq. 1) and temperature applied in the GEMM epilogue, written to
+ * args->scores, and the text-head projection of the TEXT rows reduced to
+ * per-64-column (max, lowest argmax) partials kept in the workspace.  Tokens
+ * and the grid are not touched. */
+mcd_status mcd_head_logits(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
+
+/* Second half of a step, from the scores in args->scores (same layout as
+ * above; they may come from mcd_head_logits or from the caller): selection,
+ * draw, pads, companion copy and grid scatter for the audio rows.  TEXT rows
+ * take their greedy token from the partials the last mcd_head_logits call left
+ * in the same workspace; a batch with TEXT rows must therefore follow such a
+ * call (args->hidden is not read). */
 mcd_status mcd_sample_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
 
 /* ---- delay pattern (Sec. 2.1) --------------------------------------------

@@ -282,12 +282,21 @@ mcd_status mcd_head_step(const mcd_head *h, const mcd_step_args *a, hipStream_t 
   return MCD_OK;
 }
 
+mcd_status mcd_head_logits(const mcd_head *h, const mcd_step_args *a, hipStream_t stream) {
+  mcd::StepView sv;
+  mcd_status s = make_step_view(h, a, true, sv);
+  if (s != MCD_OK) return s;
+  if (sv.R == 0) return MCD_OK;
+  hipError_t e = mcd::launch_head_gemm(h->hv, sv, stream);
+  return e == hipSuccess ? MCD_OK : hip_fail(e, "head GEMM launch");
+}
+
 mcd_status mcd_sample_step(const mcd_head *h, const mcd_step_args *a, hipStream_t stream) {
   mcd::StepView sv;
   mcd_status s = make_step_view(h, a, false, sv);
   if (s != MCD_OK) return s;
-  if (sv.Rs == 0) return MCD_OK;
-  hipError_t e = mcd::launch_sample(h->hv, sv, false, stream);
+  if (sv.R == 0) return MCD_OK;
+  hipError_t e = mcd::launch_sample(h->hv, sv, true, stream);
   if (e != hipSuccess) return hip_fail(e, "sample launch");
   return MCD_OK;
 }

@@ -85,6 +85,15 @@ class DeviceWorkload:
         mcd.mcd_head_step(self.heads[copy].handle, stream=stream,
                           **self.step_kwargs(t, self.hidden[hi]))
 
+    def run_logits(self, t: int, hidden_index=None, copy=0, stream=None):
+        hi = t if hidden_index is None else hidden_index
+        mcd.mcd_head_logits(self.heads[copy].handle, stream=stream,
+                            **self.step_kwargs(t, self.hidden[hi]))
+
+    def run_sample(self, t: int, copy=0, stream=None):
+        mcd.mcd_sample_step(self.heads[copy].handle, stream=stream,
+                            **self.step_kwargs(t, None))
+
     def sample_only(self, t: int, scores: torch.Tensor, stream=None):
         mcd.mcd_sample_step(self.heads[0].handle, stream=stream,
                             **self.step_kwargs(t, None, scores=scores))
