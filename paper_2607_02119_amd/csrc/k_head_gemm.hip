@@ -10,6 +10,8 @@
 // The unmerged logits live only in accumulator registers: a pair's two rows sit
 // in the same lane (rows 4q..4q+3 of a 16x16 MFMA block belong to one lane), so
 // the merge is a per-lane FMA.
+#include <type_traits>
+
 #include "mcd_internal.h"
 
 namespace mcd {
@@ -17,6 +19,19 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16-byte chunk in registers
+
+// Compile-time loop: f(integral_constant<int, I>) for I in [B, E).  Register
+// arrays indexed only through it keep literal indices from the first
+// optimisation pass on, so they are never demoted to scratch or LDS.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 __device__ inline bool plan_ok(const StepView &sv) {
   const int32_t *p = sv.plan;
@@ -127,20 +142,20 @@ __global__ __launch_bounds__(256) void head_gemm_bf16(HeadView hv, StepView sv) 
     boff[i] = row * LDK + col;
   }
 
-  uint4 areg[ACH], breg[BCH];
+  u32x4 areg[ACH], breg[BCH];
   auto load = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < ACH; ++i)
-      areg[i] = asrc[i] ? *reinterpret_cast<const uint4 *>(asrc[i] + kt * BK) : make_uint4(0, 0, 0, 0);
+      areg[i] = asrc[i] ? *reinterpret_cast<const u32x4 *>(asrc[i] + kt * BK) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < BCH; ++i)
-      breg[i] = bsrc[i] ? *reinterpret_cast<const uint4 *>(bsrc[i] + kt * BK) : make_uint4(0, 0, 0, 0);
+      breg[i] = bsrc[i] ? *reinterpret_cast<const u32x4 *>(bsrc[i] + kt * BK) : u32x4{0u, 0u, 0u, 0u};
   };
   auto store = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) *reinterpret_cast<uint4 *>(&As[buf][aoff[i]]) = areg[i];
+    for (int i = 0; i < ACH; ++i) *reinterpret_cast<u32x4 *>(&As[buf][aoff[i]]) = areg[i];
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) *reinterpret_cast<uint4 *>(&Bs[buf][boff[i]]) = breg[i];
+    for (int i = 0; i < BCH; ++i) *reinterpret_cast<u32x4 *>(&Bs[buf][boff[i]]) = breg[i];
   };
 
   floatx4 acc[MB][NB];
@@ -190,36 +205,374 @@ __global__ __launch_bounds__(256) void head_gemm_bf16(HeadView hv, StepView sv) 
         emit_audio(hv, sv, rows, g + 2, acc[i][j][2], acc[i][j][3], n);
       }
   } else {
-    // each wave's column half is one 64-column part
-    static_assert(BN / 2 == kTextPartCols, "text parts are 64 columns");
-    const int part = (n0 + wn * (BN / 2)) / kTextPartCols;
+    // each wave's column half is two 32-column parts (blocks j = 0,1 and 2,3)
+    static_assert(NB % 2 == 0 && kTextPartCols == 32, "text parts are 32 columns");
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int jp = 0; jp < NB; jp += 2) {
+          float bv = -INFINITY;
+          int bi = INT32_MAX;
+#pragma unroll
+          for (int j = jp; j < jp + 2; ++j) {
+            const int n = n0 + wn * (BN / 2) + j * 16 + frow;
+            if (n < N) better(bv, bi, acc[i][j][q], n);
+          }
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) {
+            const float ov = __shfl_xor(bv, off);
+            const int oi = __shfl_xor(bi, off);
+            better(bv, bi, ov, oi);
+          }
+          const int g = m0 + wm * (BM / 2) + i * 16 + rq + q;
+          const int part = (n0 + wn * (BN / 2) + jp * 16) / kTextPartCols;
+          if (frow == 0 && g < M && part < sv.text_parts) {
+            sv.text_val[(size_t)g * sv.text_parts + part] = bv;
+            sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
+          }
+        }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Weight-streaming path for up to 128 rows, staged with direct global->LDS
+// loads.  A workgroup owns all BM rows and BN columns.  Each k slice of SK = 64
+// (128 bytes of every weight and hidden row) is copied into one of S LDS
+// stages by global_load_lds_dwordx4 (64 lanes x 16 B, eight 128-byte row
+// segments per instruction), S - 1 slices ahead of its use, without passing
+// through registers.  Waves split the tile 2 x 2: column half (w & 1) and the
+// k32 half (w >> 1) of every slice; the two k halves meet in LDS at the end.
+//
+// LDS layout of a slice: [rows][8 chunks of 16 B]; chunk c of row r is stored
+// at position c ^ ((r >> 1) & 7), so the 16 rows of an MFMA fragment read hit
+// 16 distinct bank groups.  The loop waits for the copies explicitly (vector
+// memory counter: only these copies are outstanding in the loop); slices past
+// the end re-load the last slice (clamped) so that every iteration issues the
+// same count, and a copy only ever targets the stage read S - 1 iterations
+// earlier, after a barrier that follows every wave's reads of it.
+constexpr int kDmaSK = 64;                 // k per slice
+constexpr int kDmaLdsBudget = 144 * 1024;  // bytes of LDS for the two rings
+
+// s_waitcnt immediate: at most n outstanding vector-memory operations and no
+// outstanding LDS operation (gfx9 encoding; export counter left free).
+template <int n>
+__device__ __forceinline__ void wait_vmem_and_lds() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  constexpr int imm = (n & 0xF) | (0x7 << 4) | (0x0 << 8) | (((n >> 4) & 3) << 14);
+  __builtin_amdgcn_s_waitcnt(imm);
+}
+
+// 16-byte global->LDS copy per lane: lane i's 16 bytes land at LDS byte
+// address lds_base + 16 * i (lds_base is wave-uniform and goes to M0).  Issued
+// as inline assembly so that the compiler does not insert its own conservative
+// waits for it; the kernel waits for these copies explicitly.
+__device__ __forceinline__ void lds_copy16(const void *src, uint32_t lds_base) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_base) : "memory");
+}
+
+// Workgroup barrier that does not wait for outstanding global->LDS copies
+// (__syncthreads would drain them all); compiler-only fences keep memory
+// accesses on their side of it.
+__device__ __forceinline__ void block_barrier_no_vmem_wait() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int BM, int BN, bool TEXT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void head_gemm_dma(
+    HeadView hv, StepView sv) {
+  constexpr int SK = kDmaSK;
+  constexpr int MB = BM / 32;              // 32-row MFMA blocks: all rows of the tile
+  constexpr int WN = BN / 2;               // columns per wave
+  constexpr int NB = WN / 32;              // 32-column MFMA blocks per wave
+  constexpr int ROWB = SK * 2;             // bytes of one row segment (128)
+  constexpr int WST = BN * ROWB, AST = BM * ROWB;
+  // Waves 0-1 copy weight slices, waves 2-3 hidden-state slices.  Vector
+  // memory operations of one wave complete in issue order, so a wave that
+  // issued only weight copies can keep SW - 1 of them in flight without
+  // waiting behind the (faster, L2-resident) hidden-state copies.
+  constexpr int SA = 3;                                           // hidden-state stages
+  constexpr int SW0 = (kDmaLdsBudget - SA * AST) / WST;
+  constexpr int SW = SW0 > 8 ? 8 : SW0;                           // weight stages
+  constexpr int WIW = WST / 1024 / 2;      // copy instructions per weight wave per slice
+  constexpr int AIA = AST / 1024 / 2;      // per hidden-state wave per slice
+  static_assert(SW >= 3 && WIW >= 1 && AIA >= 1 && MB >= 1 && NB >= 1, "tile shape");
+  static_assert((SW - 2) * WIW < 64 && (SA - 2) * AIA < 64, "vmcnt range");
+
+  __shared__ __attribute__((aligned(1024))) char wring[SW * WST];
+  __shared__ __attribute__((aligned(1024))) char aring[SA * AST];
+  // per pair of GEMM rows (2q, 2q + 1): {w, 1/T, out, -2} for a CFG pair,
+  // {1/T_0, 1/T_1, out_0, out_1} for two solo rows (out -1: no row)
+  __shared__ float4 rowp[BM / 2];
+
+  if (!plan_ok(sv)) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    return;
+  }
+  const int32_t *rows = sv.plan + kPlanHeader + (TEXT ? sv.Mg : 0);
+  const int M = TEXT ? sv.n_text : sv.Mg;
+  const int N = TEXT ? hv.V_text : hv.N;
+  const __bf16 *Wp = static_cast<const __bf16 *>(TEXT ? hv.W_text : hv.W);
+  const __bf16 *X = static_cast<const __bf16 *>(sv.hidden);
+  const int H = hv.H;
+  const int NST = H / SK;
+
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tile_m = blockIdx.x % tiles_m;
+  const int tile_n = blockIdx.x / tiles_m;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ch = wave & 1, kh = wave >> 1;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const bool w_copier = wave_s < 2;        // wave-uniform role
+
+  if (!TEXT && tid < BM / 2) {
+    const int g0 = m0 + 2 * tid;
+    float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
+    if (g0 < 2 * sv.n_pairs) {
+      const int r = rows[g0];              // the pair's Main row carries w and T
+      if (r >= 0 && r < sv.R) {
+        const float T = sv.temperature[r];
+        pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
+                         __int_as_float(-2));
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int g = g0 + h;
+        if (g < sv.Mg) {
+          const int r = rows[g];
+          if (r >= 0 && r < sv.R) {
+            const float T = sv.temperature[r];
+            const float it = T > 0.0f ? 1.0f / T : 1.0f;
+            const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
+            if (h == 0) {
+              pr.x = it;
+              pr.z = __int_as_float(out);
+            } else {
+              pr.y = it;
+              pr.w = __int_as_float(out);
+            }
+          }
+        }
+      }
+    }
+    rowp[tid] = pr;
+  }
+
+  // Per-lane global sources of this wave's copy instructions (chunk-swizzled):
+  // a weight wave copies rows (wave * WIW + q) * 8 .. +7 of the tile, a
+  // hidden-state wave rows ((wave - 2) * AIA + q) * 8 .. +7.
+  const int seg_r = lane >> 3, seg_c = lane & 7;
+  constexpr int QN = WIW > AIA ? WIW : AIA;
+  const __bf16 *src[QN];
+  static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    src[q] = nullptr;
+    if (w_copier) {
+      if (q < WIW) {
+        const int r = (wave_s * WIW + q) * 8 + seg_r;
+        const int n = min(n0 + r, N - 1);
+        src[q] = Wp + (size_t)n * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+      }
+    } else if (q < AIA) {
+      const int r = ((wave_s - 2) * AIA + q) * 8 + seg_r;
+      int pr = rows[min(m0 + r, M - 1)];
+      if (pr < 0 || pr >= sv.R) {
+        atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+        pr = 0;
+      }
+      src[q] = X + (size_t)pr * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+    }
+  });
+
+  // Each tile walks the k slices starting at its own offset, so that at any
+  // moment the workgroups read different offsets of their (8 KiB-strided)
+  // weight rows and spread over the HBM channels instead of all hitting the
+  // same ones.  The sum order per tile is fixed, so results stay deterministic.
+  const int kskew = (int)(((unsigned)tile_n * 7u) % (unsigned)NST);
+  const uint32_t wbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)wring;
+  const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)aring;
+  // copy slice st (clamped to the last one) into its stage
+  auto issue_w = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = wbase + (uint32_t)((st % SW) * WST);
+    static_for<0, WIW>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)((wave_s * WIW + q) * 1024));
+    });
+  };
+  auto issue_a = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = abase + (uint32_t)((st % SA) * AST);
+    static_for<0, AIA>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+    });
+  };
+
+  floatx16 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Fragment byte offsets within a stage.  v_mfma_f32_32x32x16_bf16: lane l
+  // holds row (or column) l % 32 and the 8 consecutive k of chunk l / 32 of the
+  // k16 step; this wave covers k32 half kh of the slice (chunks 4kh .. 4kh+3).
+  const int frow = lane & 31;
+  int aoff[2][MB], woff[2][NB];
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const int c = 4 * kh + 2 * s2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const int r = i * 32 + frow;
+      aoff[s2][i] = r * ROWB + ((c ^ ((r >> 1) & 7)) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int r = ch * WN + j * 32 + frow;
+      woff[s2][j] = r * ROWB + ((c ^ ((r >> 1) & 7)) * 16);
+    }
+  }
+
+  wait_vmem_and_lds<0>();   // nothing but the copies may be outstanding in the loop
+  if (w_copier) {
+#pragma unroll
+    for (int st = 0; st < SW - 1; ++st) issue_w(st);
+  } else {
+#pragma unroll
+    for (int st = 0; st < SA - 1; ++st) issue_a(st);
+  }
+  for (int st = 0; st < NST; ++st) {
+    // this wave's copies of slice st have landed and its reads of slice st - 1
+    // are done; the barrier extends both to the whole workgroup
+    if (w_copier) wait_vmem_and_lds<(SW - 2) * WIW>();
+    else wait_vmem_and_lds<(SA - 2) * AIA>();
+    block_barrier_no_vmem_wait();
+    if (w_copier) issue_w(st + SW - 1);
+    else issue_a(st + SA - 1);
+    const char *wsb = wring + (st % SW) * WST;
+    const char *asb = aring + (st % SA) * AST;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      bf16x8 a[MB], b[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(asb + aoff[s2][i]);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = *reinterpret_cast<const bf16x8 *>(wsb + woff[s2][j]);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // the copies are invisible to the compiler: drain them before reusing LDS
+  wait_vmem_and_lds<0>();
+  __syncthreads();
+
+  // The two k halves exchange partial sums through LDS so that each wave ends
+  // up with the full sums of half of the tile's accumulators (flat index
+  // f = (i * NB + j) * 16 + r; wave kh keeps f in [kh * F/2, (kh + 1) * F/2)),
+  // and all four waves share the epilogue.  Two-term sums are order-free.
+  constexpr int NF = MB * NB * 16, HF = NF / 2;
+  static_assert(4 * HF * 64 * 4 <= SW * WST, "exchange area fits the weight ring");
+  float(*xch)[2][HF][64] = reinterpret_cast<float(*)[2][HF][64]>(wring);
+  static_for<0, NF>([&](auto fc) __attribute__((always_inline)) {
+    constexpr int f = decltype(fc)::value;
+    constexpr int half = f / HF;
+    if (half != kh) xch[ch][half][f % HF][lane] = acc[f / (NB * 16)][(f / 16) % NB][f % 16];
+  });
+  __syncthreads();
+  static_for<0, NF>([&](auto fc) __attribute__((always_inline)) {
+    constexpr int f = decltype(fc)::value;
+    constexpr int half = f / HF;
+    if (half == kh) acc[f / (NB * 16)][(f / 16) % NB][f % 16] += xch[ch][half][f % HF][lane];
+  });
+
+  // C layout of the 32x32 block: lane l holds column l % 32 and, in register
+  // r, row 8 * (r / 4) + 4 * (l / 32) + r % 4; the pair rows (even, odd) sit in
+  // registers r, r + 1 of the same lane.
+  const int rq = (lane >> 5) * 4;
+  auto for_my_half = [&](auto &&fn) __attribute__((always_inline)) {
+    // fn(i, j, r) for the even r of this wave's half (kh is wave-uniform)
+    static_for<0, NF / 2>([&](auto pc) __attribute__((always_inline)) {
+      constexpr int f = 2 * decltype(pc)::value;
+      constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+      if (f / HF == kh) fn(std::integral_constant<int, i>{}, std::integral_constant<int, j>{},
+                          std::integral_constant<int, r>{});
+    });
+  };
+  if constexpr (!TEXT) {
+    float bias[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int n = n0 + ch * WN + j * 32 + frow;
+      bias[j] = (hv.bias && n < N) ? hv.bias[n] : 0.0f;
+    }
+    // one instance per k half, so that every register index is a constant
+    auto epilogue = [&](auto khc) __attribute__((always_inline)) {
+      constexpr int KH = decltype(khc)::value;
+      static_for<0, HF / 2>([&](auto kc) __attribute__((always_inline)) {
+        constexpr int f = KH * HF + 2 * decltype(kc)::value;   // flat index, even r
+        constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+        const int gl = i * 32 + (r >> 2) * 8 + rq + (r & 3);   // even GEMM row within the tile
+        const int g = m0 + gl;
+        const int n = n0 + ch * WN + j * 32 + frow;
+        const float4 pr = rowp[gl >> 1];
+        const float v0 = acc[i][j][r] + bias[j], v1 = acc[i][j][r + 1] + bias[j];
+        if (g < M && n < N) {
+          const int o0 = __float_as_int(pr.z), o1 = __float_as_int(pr.w);
+          if (o1 == -2) {
+            sv.scores[(size_t)o0 * N + n] = fmaf(pr.x, v0, (1.0f - pr.x) * v1) * pr.y;
+          } else {
+            if (o0 >= 0) sv.scores[(size_t)o0 * N + n] = v0 * pr.x;
+            if (o1 >= 0) sv.scores[(size_t)o1 * N + n] = v1 * pr.y;
+          }
+        }
+      });
+    };
+    if (kh == 0) epilogue(std::integral_constant<int, 0>{});
+    else epilogue(std::integral_constant<int, 1>{});
+  } else {
+    static_assert(kTextPartCols == 32, "one 32-column block per text part");
+    for_my_half([&](auto ic, auto jc, auto rc) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value, j = decltype(jc)::value, r0 = decltype(rc)::value;
+      const int n = n0 + ch * WN + j * 32 + frow;
+      const int part = (n0 + ch * WN + j * 32) / kTextPartCols;
+#pragma unroll
+      for (int r = r0; r < r0 + 2; ++r) {
         float bv = -INFINITY;
         int bi = INT32_MAX;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + wn * (BN / 2) + j * 16 + frow;
-          if (n < N) better(bv, bi, acc[i][j][q], n);
+        if (n < N) {
+          bv = acc[i][j][r];
+          bi = n;
         }
 #pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
+        for (int off = 1; off < 32; off <<= 1) {
           const float ov = __shfl_xor(bv, off);
           const int oi = __shfl_xor(bi, off);
           better(bv, bi, ov, oi);
         }
-        const int g = m0 + wm * (BM / 2) + i * 16 + rq + q;
+        const int g = m0 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
         if (frow == 0 && g < M && part < sv.text_parts) {
           sv.text_val[(size_t)g * sv.text_parts + part] = bv;
           sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
         }
       }
+    });
   }
 }
 
-// ---------------------------------------------------------------------------
 // fp32 path (plain FMA, ascending h).  256 threads: 64 columns x 4 row lanes;
 // thread (c, y) computes column n0 + c for GEMM row pairs y, y+4, ...
 template <bool TEXT>
@@ -256,6 +609,7 @@ __global__ __launch_bounds__(256) void head_gemm_f32(HeadView hv, StepView sv) {
       emit_audio(hv, sv, rows, g, v0, v1, n);
     }
   } else {
+    // two 32-column parts per block: lanes 0-31 and 32-63
     for (int g0 = 0; g0 < M; g0 += 4) {
       const int g = g0 + y;
       float bv = -INFINITY;
@@ -264,14 +618,15 @@ __global__ __launch_bounds__(256) void head_gemm_f32(HeadView hv, StepView sv) {
         bv = dot(g);
         bi = n;
       }
-      for (int off = 1; off < 64; off <<= 1) {
+      for (int off = 1; off < 32; off <<= 1) {
         const float ov = __shfl_xor(bv, off);
         const int oi = __shfl_xor(bi, off);
         better(bv, bi, ov, oi);
       }
-      if (c == 0 && g < M) {
-        sv.text_val[(size_t)g * sv.text_parts + blockIdx.x] = bv;
-        sv.text_idx[(size_t)g * sv.text_parts + blockIdx.x] = bi;
+      const int part = blockIdx.x * 2 + (c >> 5);
+      if ((c & 31) == 0 && g < M && part < sv.text_parts) {
+        sv.text_val[(size_t)g * sv.text_parts + part] = bv;
+        sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
       }
     }
   }
@@ -282,6 +637,23 @@ hipError_t launch_bf16(const HeadView &hv, const StepView &sv, int M, int N, hip
   const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
   hipLaunchKernelGGL((head_gemm_bf16<BM, BN, TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
   return hipGetLastError();
+}
+
+template <int BM, int BN, bool TEXT>
+hipError_t launch_dma(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+  hipLaunchKernelGGL((head_gemm_dma<BM, BN, TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
+  return hipGetLastError();
+}
+
+// Weight-streaming launch for M <= 128 rows: 128-column tiles, or 64 when that
+// leaves fewer workgroups than compute units.
+template <bool TEXT>
+hipError_t launch_skinny(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  const bool narrow = (N + 127) / 128 < 256;
+  if (M <= 32) return narrow ? launch_dma<32, 64, TEXT>(hv, sv, M, N, st) : launch_dma<32, 128, TEXT>(hv, sv, M, N, st);
+  if (M <= 64) return narrow ? launch_dma<64, 64, TEXT>(hv, sv, M, N, st) : launch_dma<64, 128, TEXT>(hv, sv, M, N, st);
+  return narrow ? launch_dma<128, 64, TEXT>(hv, sv, M, N, st) : launch_dma<128, 128, TEXT>(hv, sv, M, N, st);
 }
 
 }  // namespace
@@ -301,12 +673,11 @@ hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t 
     return e;
   }
   if (sv.Mg > 0) {
-    if (sv.Mg <= 32) e = launch_bf16<32, 64, false>(hv, sv, sv.Mg, hv.N, st);
-    else if (sv.Mg <= 64) e = launch_bf16<64, 128, false>(hv, sv, sv.Mg, hv.N, st);
+    if (sv.Mg <= 128) e = launch_skinny<false>(hv, sv, sv.Mg, hv.N, st);
     else e = launch_bf16<128, 128, false>(hv, sv, sv.Mg, hv.N, st);
   }
   if (e == hipSuccess && sv.n_text > 0) {
-    if (sv.n_text <= 64) e = launch_bf16<64, 128, true>(hv, sv, sv.n_text, hv.V_text, st);
+    if (sv.n_text <= 128) e = launch_skinny<true>(hv, sv, sv.n_text, hv.V_text, st);
     else e = launch_bf16<128, 128, true>(hv, sv, sv.n_text, hv.V_text, st);
   }
   return e;

@@ -16,9 +16,9 @@ enum { kPlanMagicWord = 0, kPlanR = 1, kPlanPairs = 2, kPlanSolo = 3, kPlanText 
 
 constexpr int kStatusBytes = 256;  // status word region at the start of the workspace
 
-// Columns of a text-head tile; the text GEMM writes one (max, argmax) partial per
-// row for every kTextPartCols columns.
-constexpr int kTextPartCols = 64;
+// The text GEMM writes one (max, lowest argmax) partial per row for every
+// kTextPartCols columns of the text vocabulary.
+constexpr int kTextPartCols = 32;
 
 struct Delays {
   int32_t d[MCD_MAX_K];

@@ -96,6 +96,13 @@ RAGGED = [
                                dtype="bf16", top_k=7, temperature=0.7, steps=6, shuffle=True)),
     ("bf16_topp_two_tiles", dict(H=192, K=2, V=333, n_pairs=20, n_solo=3, dtype="bf16",
                                  top_p=0.9, cfg_w=2.0, steps=4)),
+    # H % 256 == 0 and at most 128 rows: the weight-streaming kernel (32/64/128-row tiles)
+    ("stream_bm32_text", dict(H=256, K=3, V=37, n_pairs=10, n_solo=5, n_text=3, V_text=300,
+                              dtype="bf16", top_k=7, temperature=0.7, steps=5, shuffle=True)),
+    ("stream_bm64", dict(H=512, K=2, V=333, n_pairs=25, n_solo=3, n_text=40, V_text=1000,
+                         dtype="bf16", top_p=0.9, cfg_w=2.0, steps=4, shuffle=True)),
+    ("stream_bm128", dict(H=768, K=4, V=129, n_pairs=55, n_solo=3, n_text=100, V_text=515,
+                          dtype="bf16", top_k=20, steps=5)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
                               dtype="f32", top_k=5, top_p=0.8, steps=5, shuffle=True)),
     ("bf16_greedy", dict(H=64, K=4, V=100, n_pairs=5, n_solo=4, dtype="bf16", temperature=0.0,
