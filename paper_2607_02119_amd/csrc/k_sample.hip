@@ -15,17 +15,21 @@
 //     request's frame grid cell [k][f].
 //
 // Selection is a radix select over order-preserving 32-bit keys of the fp32
-// scores (four 8-bit digit passes, histograms in LDS).  Top-k histograms count
-// elements; top-p histograms add fixed-point masses round(exp(s - max) * 2^48)
-// as 64-bit integers, so the sums are exact and independent of the order in
-// which lanes add them.
+// scores (8-bit digits from the top, histograms in LDS).  Top-k histograms
+// count elements and stop as soon as the bucket holding the cut is taken whole;
+// top-p histograms add fixed-point masses exp(s - max) * 2^48 (fp32 exp,
+// converted exactly) as 64-bit integers, so the sums are exact and independent
+// of the order of the adds.
+// Three rotating histogram buffers need one barrier per digit pass: every wave
+// scans the whole histogram itself, so no result has to be broadcast.
 #include "mcd_internal.h"
 
 namespace mcd {
 namespace {
 
 constexpr int kWave = 64;
-constexpr double kMassScale = 281474976710656.0;  // 2^48
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
 
 __device__ inline uint32_t order_key(float x) {
   if (x == 0.0f) x = 0.0f;  // -0 and +0 compare equal
@@ -39,23 +43,14 @@ __device__ inline bool plan_ok(const StepView &sv) {
          p[kPlanSolo] == sv.n_solo && p[kPlanText] == sv.n_text;
 }
 
-// ---- block-level helpers (one 256-thread block per vector) ------------------
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-
 template <int EPL>
 struct Smem {
-  uint32_t hc[256];
-  unsigned long long hm[256];
-  unsigned long long u64[kWaves];
-  float f32[kWaves];
-  double f64[kWaves];
-  int i32[kWaves];
-  uint32_t cnt[EPL * kWaves];
-  int bc_digit;
-  unsigned long long bc_above;
-  int n_kept;
-  uint16_t klist[EPL * kThreads];
+  unsigned long long hist[3][256];   // rotating digit histograms (counts or masses)
+  unsigned long long r64[2][kWaves];  // block reductions (double-buffered)
+  double rf[2][kWaves];
+  int ri[2][kWaves];
+  uint32_t cnt[EPL * kWaves];         // tie counts per (element slot, wave)
+  uint32_t kept[(EPL * kThreads + 31) / 32];  // kept-id bitmask
 };
 
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
@@ -74,51 +69,38 @@ __device__ inline void keep_better(T &bv, int &bi, T v, int i) {
   }
 }
 
+// Block reductions; `slot` alternates between consecutive calls so that one
+// barrier suffices (the buffer written now was last read two calls ago).
 template <int EPL>
-__device__ inline uint64_t block_sum_u64(uint64_t x, Smem<EPL> &sm) {
+__device__ inline uint64_t block_sum_u64(uint64_t x, Smem<EPL> &sm, int slot) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
-  if (lane_id() == 0) sm.u64[wave_id()] = x;
+  if (lane_id() == 0) sm.r64[slot][wave_id()] = x;
   __syncthreads();
   uint64_t r = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r += sm.u64[w];
-  __syncthreads();
+  for (int w = 0; w < kWaves; ++w) r += sm.r64[slot][w];
   return r;
 }
 
 template <int EPL>
-__device__ inline uint64_t block_max_u64(uint64_t x, Smem<EPL> &sm) {
+__device__ inline uint64_t block_max_u64(uint64_t x, Smem<EPL> &sm, int slot) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const uint64_t o = __shfl_xor(x, off);
     x = o > x ? o : x;
   }
-  if (lane_id() == 0) sm.u64[wave_id()] = x;
+  if (lane_id() == 0) sm.r64[slot][wave_id()] = x;
   __syncthreads();
   uint64_t r = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = sm.u64[w] > r ? sm.u64[w] : r;
-  __syncthreads();
-  return r;
-}
-
-template <int EPL>
-__device__ inline float block_max_f32(float x, Smem<EPL> &sm) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
-  if (lane_id() == 0) sm.f32[wave_id()] = x;
-  __syncthreads();
-  float r = sm.f32[0];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) r = fmaxf(r, sm.f32[w]);
-  __syncthreads();
+  for (int w = 0; w < kWaves; ++w) r = sm.r64[slot][w] > r ? sm.r64[slot][w] : r;
   return r;
 }
 
 // (value desc, id asc) maximum over the block; every thread gets the id.
 template <typename T, int EPL>
-__device__ inline int block_argmax(T bv, int bi, Smem<EPL> &sm) {
+__device__ inline int block_argmax(T bv, int bi, Smem<EPL> &sm, int slot) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const T ov = __shfl_xor(bv, off);
@@ -126,23 +108,26 @@ __device__ inline int block_argmax(T bv, int bi, Smem<EPL> &sm) {
     keep_better(bv, bi, ov, oi);
   }
   if (lane_id() == 0) {
-    sm.f64[wave_id()] = (double)bv;
-    sm.i32[wave_id()] = bi;
+    sm.rf[slot][wave_id()] = (double)bv;
+    sm.ri[slot][wave_id()] = bi;
   }
   __syncthreads();
-  double rv = sm.f64[0];
-  int ri = sm.i32[0];
+  double rv = sm.rf[slot][0];
+  int ri = sm.ri[slot][0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.f64[w], sm.i32[w]);
-  __syncthreads();
+  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rf[slot][w], sm.ri[slot][w]);
   return ri;
 }
 
 // ---- Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11) ---------------------
-__device__ inline uint64_t philox_word(uint64_t seed, uint64_t key, uint64_t t, uint64_t k,
-                                       uint32_t v) {
+struct U64x4 {
+  uint64_t w[4];
+};
+
+__device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, uint64_t k,
+                                     uint64_t group) {
   const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
-  uint64_t x0 = v >> 2, x1 = k, x2 = t, x3 = key;
+  uint64_t x0 = group, x1 = k, x2 = t, x3 = key;
   uint64_t k0 = seed, k1 = 0;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
@@ -158,110 +143,141 @@ __device__ inline uint64_t philox_word(uint64_t seed, uint64_t key, uint64_t t, 
     x2 = y2;
     x3 = lo0;
   }
-  switch (v & 3) {
-    case 0: return x0;
-    case 1: return x1;
-    case 2: return x2;
-    default: return x3;
-  }
+  return U64x4{{x0, x1, x2, x3}};
 }
 
-__device__ inline double gumbel(uint64_t seed, uint64_t key, uint64_t t, uint64_t k, uint32_t v) {
-  const uint64_t x = philox_word(seed, key, t, k, v);
-  const double u = ((double)(x >> 41) + 0.5) * 0x1p-23;
-  return -log(-log(u));
+// Gumbel variate from one Philox word, in fp32 (the uniform is exact in fp32;
+// each log is within about one ulp, so G is within ~1e-6 of its exact value).
+__device__ inline float gumbel_from_word(uint64_t x) {
+  const float u = ((float)(uint32_t)(x >> 41) + 0.5f) * 0x1p-23f;
+  return -logf(-logf(u));
 }
 
 // ---- radix select ------------------------------------------------------------
-// Finds the boundary key kappa of the "take `target` units from the top" cut
-// among active elements (units: 1 per element, or its fixed-point mass) and the
-// amount `rem` (>= 1) still to take from the elements whose key == kappa.
-// Returns false if the active total is below target (then everything is kept).
-// Element i of thread tid is id e = i*256 + tid.
+// Cut of "take `target` units from the top" among the active elements (units:
+// 1 per element, or its fixed-point mass).  Result: keep every active element
+// with key >= lo; when `exact`, lo is a single key kappa whose ties are kept
+// only up to `need` units (ties carry equal units) -- see apply_cut.
+struct Cut {
+  uint32_t lo;
+  bool exact;
+  uint64_t need;   // units still wanted from the elements with key == lo (exact only)
+  bool all;        // target not reached: keep every active element
+};
+
+// Element i of thread tid is id e = i*256 + tid.  `pass` counts the digit
+// passes done so far in this vector and selects the rotating buffers; the
+// buffers pass % 3 and (pass + 1) % 3 must be zero on entry, and the two after
+// the last one used are zero again on exit.
 template <int EPL, bool MASS>
-__device__ bool radix_select(const float (&x)[EPL], uint32_t active, const uint64_t *mass,
-                             uint64_t target, Smem<EPL> &sm, uint32_t &kappa, uint64_t &rem) {
-  const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+__device__ Cut radix_select(const float (&x)[EPL], uint32_t active, const uint64_t *mass,
+                            uint64_t target, Smem<EPL> &sm, int &pass) {
+  const int tid = threadIdx.x, lane = lane_id();
   uint32_t prefix = 0, pmask = 0;
-  rem = target;
+  uint64_t rem = target;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    if (MASS) sm.hm[tid] = 0;
-    else sm.hc[tid] = 0;
-    if (tid == 0) sm.bc_digit = -1;
-    __syncthreads();
+    unsigned long long *h = sm.hist[pass % 3];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
       const uint32_t key = order_key(x[i]);
       if (((active >> i) & 1) && (key & pmask) == prefix) {
         const uint32_t d = (key >> shift) & 255u;
-        if (MASS) atomicAdd(&sm.hm[d], (unsigned long long)mass[i]);
-        else atomicAdd(&sm.hc[d], 1u);
+        atomicAdd(&h[d], MASS ? (unsigned long long)mass[i] : 1ull);
       }
     }
     __syncthreads();
-    // thread t owns digit 255 - t: scanning threads in order walks digits downwards
-    const int d = 255 - tid;
-    const uint64_t v = MASS ? (uint64_t)sm.hm[d] : (uint64_t)sm.hc[d];
-    uint64_t incl = v;
+    // every wave scans all 256 digits (lane l: digits 255-4l .. 252-4l)
+    uint64_t v[4], lsum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = h[255 - 4 * lane - j];
+      lsum += v[j];
+    }
+    uint64_t incl = lsum;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
       const uint64_t o = __shfl_up(incl, off);
       if (lane >= off) incl += o;
     }
-    if (lane == kWave - 1) sm.u64[wave] = incl;
-    __syncthreads();
-    for (int w = 0; w < wave; ++w) incl += sm.u64[w];
-    const uint64_t excl = incl - v;
-    if (excl < rem && incl >= rem) {
-      sm.bc_digit = d;
-      sm.bc_above = excl;
+    const uint64_t excl = incl - lsum;
+    // clear the buffer of the pass after next (its last readers passed the barrier above)
+    sm.hist[(pass + 2) % 3][tid] = 0;
+    ++pass;
+    const uint64_t bal = __ballot(excl < rem && incl >= rem);
+    if (bal == 0) return Cut{0u, false, 0, true};
+    const int src = __ffsll((long long)bal) - 1;
+    int dsel = 0;
+    uint64_t above = 0, inbucket = 0;
+    if (lane == src) {
+      uint64_t cum = excl;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (cum + v[j] >= rem) {
+          dsel = 255 - 4 * lane - j;
+          above = cum;
+          inbucket = v[j];
+          break;
+        }
+        cum += v[j];
+      }
     }
-    __syncthreads();
-    const int dsel = sm.bc_digit;
-    const uint64_t above = sm.bc_above;
-    __syncthreads();
-    if (dsel < 0) return false;
+    dsel = __shfl(dsel, src);
+    above = __shfl(above, src);
+    inbucket = __shfl(inbucket, src);
     rem -= above;
     prefix |= (uint32_t)dsel << shift;
     pmask |= 255u << shift;
+    if (!MASS && inbucket == rem) {
+      // the whole bucket is taken: keep every key whose leading digits are >= prefix
+      return Cut{prefix, false, 0, false};
+    }
   }
-  kappa = prefix;
-  return true;
+  return Cut{prefix, true, rem, false};
 }
 
-// Keep, among the active elements with key == kappa, the `need` lowest ids, and
-// every active element above kappa; drop the rest.
+// Apply a cut to the active set.  For an exact cut with fewer than all of the
+// ties at kappa wanted, the `need_n` lowest ids among the ties are kept.
 template <int EPL>
-__device__ uint32_t apply_cut(const float (&x)[EPL], uint32_t active, uint32_t kappa,
-                              uint64_t need, Smem<EPL> &sm) {
-  const int lane = lane_id(), wave = wave_id();
-  uint64_t ball[EPL];
+__device__ uint32_t apply_cut(const float (&x)[EPL], uint32_t active, const Cut &c,
+                              uint64_t need_n, Smem<EPL> &sm, int &slot) {
+  if (c.all) return active;
+  uint32_t keep = 0, ties = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    const bool tie = ((active >> i) & 1) && order_key(x[i]) == kappa;
-    ball[i] = __ballot(tie);
-    if (lane == 0) sm.cnt[i * kWaves + wave] = __popcll(ball[i]);
+    const uint32_t key = order_key(x[i]);
+    const bool act = (active >> i) & 1;
+    if (act && key >= c.lo && !(c.exact && key == c.lo)) keep |= 1u << i;
+    if (act && c.exact && key == c.lo) ties |= 1u << i;
+  }
+  if (!c.exact) return keep;
+  const uint64_t total = block_sum_u64((uint64_t)__popc(ties), sm, slot);
+  slot ^= 1;
+  if (need_n >= total) return keep | ties;
+  // rare: rank the ties by id (e = i*256 + tid)
+  const int lane = lane_id(), wave = wave_id();
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const uint64_t b = __ballot((ties >> i) & 1);
+    if (lane == 0) sm.cnt[i * kWaves + wave] = __popcll(b);
   }
   __syncthreads();
-  uint32_t out = 0;
   uint64_t base = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    uint64_t before = 0, total = 0;
+    const uint64_t b = __ballot((ties >> i) & 1);
+    uint64_t before = 0, tot = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const uint32_t c = sm.cnt[i * kWaves + w];
-      if (w < wave) before += c;
-      total += c;
+      const uint32_t cw = sm.cnt[i * kWaves + w];
+      if (w < wave) before += cw;
+      tot += cw;
     }
-    const bool act = (active >> i) & 1;
-    const uint32_t key = order_key(x[i]);
-    const uint64_t rank = base + before + __popcll(ball[i] & lanemask_lt());
-    if (act && (key > kappa || (key == kappa && rank < need))) out |= 1u << i;
-    base += total;
+    const uint64_t rank = base + before + __popcll(b & lanemask_lt());
+    if (((ties >> i) & 1) && rank < need_n) keep |= 1u << i;
+    base += tot;
   }
-  __syncthreads();
-  return out;
+  __syncthreads();  // cnt may be reused
+  return keep;
 }
 
 template <int EPL>
@@ -279,69 +295,88 @@ __device__ int select_and_draw(const HeadView &hv, const StepView &sv, const flo
     x[i] = (e < V) ? sc[e] : -INFINITY;
     if (e < V) active |= 1u << i;
   }
+  int slot = 0;
   if (greedy) {
     float bv = -INFINITY;
     int bi = INT32_MAX;
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if ((active >> i) & 1) keep_better(bv, bi, x[i], i * kThreads + tid);
-    return block_argmax(bv, bi, sm);
+    return block_argmax(bv, bi, sm, slot);
   }
+  // histograms 0 and 1 zero, kept mask zero
+#pragma unroll
+  for (int b = 0; b < 2; ++b) sm.hist[b][tid] = 0;
+  for (int w = tid; w < (EPL * kThreads + 31) / 32; w += kThreads) sm.kept[w] = 0;
+  __syncthreads();
+  int pass = 0;
   if (top_k > 0 && top_k < V) {
-    uint32_t kappa;
-    uint64_t rem;
-    if (radix_select<EPL, false>(x, active, nullptr, (uint64_t)top_k, sm, kappa, rem))
-      active = apply_cut<EPL>(x, active, kappa, rem, sm);
+    const Cut c = radix_select<EPL, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
+    active = apply_cut<EPL>(x, active, c, c.need, sm, slot);
   }
   if (top_p < 1.0f) {
     float mloc = -INFINITY;
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if ((active >> i) & 1) mloc = fmaxf(mloc, x[i]);
-    const double mx = (double)block_max_f32(mloc, sm);
+    // the max through the order key (monotone), reduced as an integer
+    const uint32_t mk = (uint32_t)block_max_u64((uint64_t)order_key(mloc), sm, slot);
+    slot ^= 1;
+    const uint32_t mu = (mk & 0x80000000u) ? (mk & 0x7FFFFFFFu) : ~mk;
+    const float mx = __uint_as_float(mu);
+    // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
+    // converted exactly to a 64-bit integer
     uint64_t mass[EPL];
     uint64_t zl = 0;
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
-      mass[i] = 0;
-      if ((active >> i) & 1) mass[i] = (uint64_t)rint(exp((double)x[i] - mx) * kMassScale);
+      mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
       zl += mass[i];
     }
-    const uint64_t Z = block_sum_u64(zl, sm);
+    const uint64_t Z = block_sum_u64(zl, sm, slot);
+    slot ^= 1;
     uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
     if (target < 1) target = 1;
     if (target <= Z) {
-      uint32_t kappa;
-      uint64_t rem;
-      if (radix_select<EPL, true>(x, active, mass, target, sm, kappa, rem)) {
-        // every element tied at kappa carries the same mass q: take the fewest reaching rem
+      const Cut c = radix_select<EPL, true>(x, active, mass, target, sm, pass);
+      uint64_t need_n = 0;
+      if (c.exact) {
+        // every element tied at kappa carries the same mass q: the fewest reaching rem
         uint64_t q = 0;
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
-          if (((active >> i) & 1) && order_key(x[i]) == kappa) q = mass[i];
-        q = block_max_u64(q, sm);
-        const uint64_t need = q ? (rem + q - 1) / q : 1;
-        active = apply_cut<EPL>(x, active, kappa, need, sm);
+          if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass[i];
+        q = block_max_u64(q, sm, slot);
+        slot ^= 1;
+        need_n = q ? (c.need + q - 1) / q : 1;
       }
+      active = apply_cut<EPL>(x, active, c, need_n, sm, slot);
     }
   }
-  // compact the kept ids (any order: the draw's tie rule makes it order-free)
-  if (tid == 0) sm.n_kept = 0;
-  __syncthreads();
+  // kept-id bitmask, then one Philox block per group of 4 consecutive ids
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if ((active >> i) & 1) sm.klist[atomicAdd(&sm.n_kept, 1)] = (uint16_t)(i * kThreads + tid);
+    if ((active >> i) & 1) {
+      const int e = i * kThreads + tid;
+      atomicOr(&sm.kept[e >> 5], 1u << (e & 31));
+    }
   __syncthreads();
-  const int n_kept = sm.n_kept;
   double bv = -INFINITY;
   int bi = INT32_MAX;
-  for (int c = tid; c < n_kept; c += kThreads) {
-    const int v = sm.klist[c];
-    const double val =
-        (double)sc[v] + gumbel(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint32_t)v);
-    keep_better(bv, bi, val, v);
+  const int groups = (V + 3) >> 2;
+  for (int g = tid; g < groups; g += kThreads) {
+    const uint32_t bits = (sm.kept[g >> 3] >> ((g & 7) * 4)) & 0xFu;
+    if (!bits) continue;
+    const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if ((bits >> j) & 1) {
+        const int v = 4 * g + j;
+        const double val = (double)sc[v] + (double)gumbel_from_word(w.w[j]);
+        keep_better(bv, bi, val, v);
+      }
   }
-  return block_argmax(bv, bi, sm);
+  return block_argmax(bv, bi, sm, slot);
 }
 
 template <int EPL>
@@ -370,7 +405,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     for (int p = tid; p < sv.text_parts; p += kThreads)
       keep_better(bv, bi, sv.text_val[(size_t)j * sv.text_parts + p],
                   sv.text_idx[(size_t)j * sv.text_parts + p]);
-    const int tok = block_argmax(bv, bi, sm);
+    const int tok = block_argmax(bv, bi, sm, 0);
     for (int k = tid; k < hv.K; k += kThreads)
       sv.tokens_out[(size_t)r * hv.K + k] = (k == 0) ? tok : hv.pad_id;
     return;

