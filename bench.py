@@ -34,6 +34,17 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector
 MALL_BYTES = 256 * 2**20       # Infinity Cache
+COPY_PROBE_BYTES = 2**30       # --copy-probe: one plain device copy of this many bytes
+
+# HBM traffic of the head projection kernel per launch, from two rocprofv3 --pmc
+# passes (FETCH_SIZE, then WRITE_SIZE) over `bench.py --copy-probe`, each
+# counter scaled by what it reads for the probe's plain copy of known size.
+# Valid only for the kernel source it was taken on (sha256 below); a changed
+# kernel reports traffic null until the counters are taken again.
+K1_SOURCE = os.path.join(ROOT, "paper_2607_02119_amd", "csrc", "k_head_gemm.hip")
+MEASURED_TRAFFIC = {
+    # workload: dict(k1_sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
+}
 
 
 def algorithmic(wl):
@@ -45,6 +56,32 @@ def algorithmic(wl):
     flops = 2.0 * Mg * wl.N * wl.H + 2.0 * wl.n_text * wl.V_text * wl.H
     return dict(weight_bytes=w_bytes, hidden_bytes=hid, bytes=w_bytes + hid, flops=flops,
                 scores_bytes=4 * wl.Rs * wl.N)
+
+
+def k1_traffic(workload):
+    """Measured HBM bytes per head-projection launch, or None if not measured
+    for this workload or the kernel source changed since."""
+    import hashlib
+    m = MEASURED_TRAFFIC.get(workload)
+    if not m:
+        return None
+    with open(K1_SOURCE, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != m["k1_sha256"]:
+            return None
+    return m["fetch_bytes"] + m["write_bytes"]
+
+
+def copy_probe(torch):
+    """A plain device copy of known size (read and write COPY_PROBE_BYTES each),
+    the calibration point for the FETCH_SIZE / WRITE_SIZE counters."""
+    n = COPY_PROBE_BYTES // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def cpu_baseline(wl, budget_s=15.0):
@@ -95,6 +132,8 @@ def main():
                     help="weight copies rotated per step (0: enough to exceed 3x the MALL)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run a plain 1 GiB device copy first (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -109,6 +148,8 @@ def main():
     alg = algorithmic(wl)
     copies = args.weight_copies or max(1, math.ceil(3 * MALL_BYTES / alg["weight_bytes"]))
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        copy_probe(torch)
     dw = harness.DeviceWorkload(wl, weight_copies=copies)
     n_hidden = min(wl.steps, args.steps + args.warmup)
     dw.load_hidden(range(n_hidden))
@@ -132,16 +173,16 @@ def main():
     ms_step = ev0.elapsed_time(ev1) / args.steps
     status |= dw.status()
 
-    # per-launch durations of the two kernels, events around each launch
+    # mean launch duration of each of the two kernels: the same steps launched
+    # back to back on the launch stream, HIP events at both ends
     def per_launch(fn):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.steps)]
-        for i, (a, b) in enumerate(evs):
-            a.record(stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(args.steps):
             fn(args.warmup + i)
-            b.record(stream)
+        b.record(stream)
         torch.cuda.synchronize()
-        return sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+        return a.elapsed_time(b) / args.steps
 
     def logits(i):
         t = i % n_hidden
@@ -165,7 +206,7 @@ def main():
         ach = alg["bytes"] / (ms_k1 * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(ach / HBM_PEAK_GBS, 4))
-    roof.update(traffic=None, kernel="head_gemm (mcd_head_logits)",
+    roof.update(traffic=k1_traffic(wl.name), kernel="head_gemm (mcd_head_logits)",
                 us_per_launch=round(ms_k1 * 1e3, 2),
                 algorithmic_bytes=alg["bytes"], algorithmic_flops=alg["flops"])
     out = {

@@ -272,6 +272,13 @@ __device__ __forceinline__ void lds_copy16(const void *src, uint32_t lds_base) {
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_base) : "memory");
 }
 
+// The same copy with the non-temporal hint, for data read exactly once (the
+// weights): it is not kept in L2 at the expense of the hidden states, which
+// every workgroup re-reads.
+__device__ __forceinline__ void lds_copy16_stream(const void *src, uint32_t lds_base) {
+  asm volatile("global_load_lds_dwordx4 %0, off nt" ::"v"(src), "{m0}"(lds_base) : "memory");
+}
+
 // Workgroup barrier that does not wait for outstanding global->LDS copies
 // (__syncthreads would drain them all); compiler-only fences keep memory
 // accesses on their side of it.
@@ -302,16 +309,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   static_assert(SW >= 3 && WIW >= 1 && AIA >= 1 && MB >= 1 && NB >= 1, "tile shape");
   static_assert((SW - 2) * WIW < 64 && (SA - 2) * AIA < 64, "vmcnt range");
 
-  __shared__ __attribute__((aligned(1024))) char wring[SW * WST];
-  __shared__ __attribute__((aligned(1024))) char aring[SA * AST];
+  __shared__ __attribute__((aligned(1024))) char lds[SW * WST + SA * AST];
+  char *const wring = lds;                 // weight stages
+  char *const aring = lds + SW * WST;      // hidden-state stages
   // per pair of GEMM rows (2q, 2q + 1): {w, 1/T, out, -2} for a CFG pair,
   // {1/T_0, 1/T_1, out_0, out_1} for two solo rows (out -1: no row)
   __shared__ float4 rowp[BM / 2];
 
-  if (!plan_ok(sv)) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-    return;
-  }
   const int32_t *rows = sv.plan + kPlanHeader + (TEXT ? sv.Mg : 0);
   const int M = TEXT ? sv.n_text : sv.Mg;
   const int N = TEXT ? hv.V_text : hv.N;
@@ -329,66 +333,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const bool w_copier = wave_s < 2;        // wave-uniform role
 
-  if (!TEXT && tid < BM / 2) {
-    const int g0 = m0 + 2 * tid;
-    float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
-    if (g0 < 2 * sv.n_pairs) {
-      const int r = rows[g0];              // the pair's Main row carries w and T
-      if (r >= 0 && r < sv.R) {
-        const float T = sv.temperature[r];
-        pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
-                         __int_as_float(-2));
-      }
-    } else {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int g = g0 + h;
-        if (g < sv.Mg) {
-          const int r = rows[g];
-          if (r >= 0 && r < sv.R) {
-            const float T = sv.temperature[r];
-            const float it = T > 0.0f ? 1.0f / T : 1.0f;
-            const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
-            if (h == 0) {
-              pr.x = it;
-              pr.z = __int_as_float(out);
-            } else {
-              pr.y = it;
-              pr.w = __int_as_float(out);
-            }
-          }
-        }
-      }
-    }
-    rowp[tid] = pr;
-  }
-
-  // Per-lane global sources of this wave's copy instructions (chunk-swizzled):
-  // a weight wave copies rows (wave * WIW + q) * 8 .. +7 of the tile, a
-  // hidden-state wave rows ((wave - 2) * AIA + q) * 8 .. +7.
-  const int seg_r = lane >> 3, seg_c = lane & 7;
-  constexpr int QN = WIW > AIA ? WIW : AIA;
-  const __bf16 *src[QN];
-  static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
-    constexpr int q = decltype(qc)::value;
-    src[q] = nullptr;
-    if (w_copier) {
-      if (q < WIW) {
-        const int r = (wave_s * WIW + q) * 8 + seg_r;
-        const int n = min(n0 + r, N - 1);
-        src[q] = Wp + (size_t)n * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
-      }
-    } else if (q < AIA) {
-      const int r = ((wave_s - 2) * AIA + q) * 8 + seg_r;
-      int pr = rows[min(m0 + r, M - 1)];
-      if (pr < 0 || pr >= sv.R) {
-        atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-        pr = 0;
-      }
-      src[q] = X + (size_t)pr * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
-    }
-  });
-
   // Each tile walks the k slices starting at its own offset, so that at any
   // moment the workgroups read different offsets of their (8 KiB-strided)
   // weight rows and spread over the HBM channels instead of all hitting the
@@ -396,6 +340,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int kskew = (int)(((unsigned)tile_n * 7u) % (unsigned)NST);
   const uint32_t wbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)wring;
   const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)aring;
+  const int seg_r = lane >> 3, seg_c = lane & 7;
+
+  // Per-lane global sources of this wave's copy instructions (chunk-swizzled):
+  // a weight wave copies rows (wave * WIW + q) * 8 .. +7 of the tile, a
+  // hidden-state wave rows ((wave - 2) * AIA + q) * 8 .. +7.
+  constexpr int QN = WIW > AIA ? WIW : AIA;
+  const __bf16 *src[QN];
   // copy slice st (clamped to the last one) into its stage
   auto issue_w = [&](int st) __attribute__((always_inline)) {
     int ks = min(st, NST - 1) + kskew;
@@ -403,7 +354,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const uint32_t sb = wbase + (uint32_t)((st % SW) * WST);
     static_for<0, WIW>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
-      lds_copy16(src[q] + ks * SK, sb + (uint32_t)((wave_s * WIW + q) * 1024));
+      lds_copy16_stream(src[q] + ks * SK, sb + (uint32_t)((wave_s * WIW + q) * 1024));
     });
   };
   auto issue_a = [&](int st) __attribute__((always_inline)) {
@@ -415,6 +366,86 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
     });
   };
+
+  // The weight waves start streaming at once: their copies depend on nothing
+  // but the tile, and nothing else is outstanding in their counters until the
+  // end of the loop.
+  wait_vmem_and_lds<0>();
+  if (w_copier) {
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < WIW) {
+        const int r = (wave_s * WIW + q) * 8 + seg_r;
+        const int n = min(n0 + r, N - 1);
+        src[q] = Wp + (size_t)n * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+      }
+    });
+#pragma unroll
+    for (int st = 0; st < SW - 1; ++st) issue_w(st);
+  }
+
+  if (!plan_ok(sv)) {
+    wait_vmem_and_lds<0>();  // no copy may still be landing in this workgroup's LDS
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    return;
+  }
+
+  if (!w_copier) {
+    // The hidden-state waves gather their rows through the plan, stage the
+    // per-row epilogue parameters in LDS, and wait for all of it before their
+    // first copy, so that only copies are outstanding in their loop counters.
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < AIA) {
+        const int r = ((wave_s - 2) * AIA + q) * 8 + seg_r;
+        int pr = rows[min(m0 + r, M - 1)];
+        if (pr < 0 || pr >= sv.R) {
+          atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+          pr = 0;
+        }
+        src[q] = X + (size_t)pr * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+      }
+    });
+    const int q2 = tid - 128;
+    if (!TEXT && q2 < BM / 2) {
+      const int g0 = m0 + 2 * q2;
+      float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
+      if (g0 < 2 * sv.n_pairs) {
+        const int r = rows[g0];              // the pair's Main row carries w and T
+        if (r >= 0 && r < sv.R) {
+          const float T = sv.temperature[r];
+          pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
+                           __int_as_float(-2));
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int g = g0 + h;
+          if (g < sv.Mg) {
+            const int r = rows[g];
+            if (r >= 0 && r < sv.R) {
+              const float T = sv.temperature[r];
+              const float it = T > 0.0f ? 1.0f / T : 1.0f;
+              const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
+              if (h == 0) {
+                pr.x = it;
+                pr.z = __int_as_float(out);
+              } else {
+                pr.y = it;
+                pr.w = __int_as_float(out);
+              }
+            }
+          }
+        }
+      }
+      rowp[q2] = pr;
+    }
+    wait_vmem_and_lds<0>();
+#pragma unroll
+    for (int st = 0; st < SA - 1; ++st) issue_a(st);
+  }
 
   floatx16 acc[MB][NB];
 #pragma unroll
@@ -444,14 +475,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   }
 
-  wait_vmem_and_lds<0>();   // nothing but the copies may be outstanding in the loop
-  if (w_copier) {
-#pragma unroll
-    for (int st = 0; st < SW - 1; ++st) issue_w(st);
-  } else {
-#pragma unroll
-    for (int st = 0; st < SA - 1; ++st) issue_a(st);
-  }
   for (int st = 0; st < NST; ++st) {
     // this wave's copies of slice st have landed and its reads of slice st - 1
     // are done; the barrier extends both to the whole workgroup
@@ -480,96 +503,94 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   wait_vmem_and_lds<0>();
   __syncthreads();
 
-  // The two k halves exchange partial sums through LDS so that each wave ends
-  // up with the full sums of half of the tile's accumulators (flat index
-  // f = (i * NB + j) * 16 + r; wave kh keeps f in [kh * F/2, (kh + 1) * F/2)),
-  // and all four waves share the epilogue.  Two-term sums are order-free.
-  constexpr int NF = MB * NB * 16, HF = NF / 2;
-  static_assert(4 * HF * 64 * 4 <= SW * WST, "exchange area fits the weight ring");
-  float(*xch)[2][HF][64] = reinterpret_cast<float(*)[2][HF][64]>(wring);
-  static_for<0, NF>([&](auto fc) __attribute__((always_inline)) {
+  // Epilogue, in two phases through LDS (the rings are free now).
+  // Phase 1: every wave writes its partial sums (its k half) to C[kh][row][col].
+  // Phase 2: each thread takes 16-byte column chunks (audio) or 32-column text
+  // parts of whole rows, adds the two k halves (a two-term sum: order-free),
+  // and applies the fused epilogue with coalesced stores.  No global load is
+  // left pending among the stores, so they never wait for each other.
+  constexpr int CP = BN + 4;               // padded row pitch of C (floats)
+  static_assert(2 * BM * CP * 4 <= SW * WST + SA * AST, "C fits the rings");
+  float *C = reinterpret_cast<float *>(lds);
+  static_for<0, MB * NB * 16>([&](auto fc) __attribute__((always_inline)) {
     constexpr int f = decltype(fc)::value;
-    constexpr int half = f / HF;
-    if (half != kh) xch[ch][half][f % HF][lane] = acc[f / (NB * 16)][(f / 16) % NB][f % 16];
-  });
-  __syncthreads();
-  static_for<0, NF>([&](auto fc) __attribute__((always_inline)) {
-    constexpr int f = decltype(fc)::value;
-    constexpr int half = f / HF;
-    if (half == kh) acc[f / (NB * 16)][(f / 16) % NB][f % 16] += xch[ch][half][f % HF][lane];
+    constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+    const int row = i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    C[(kh * BM + row) * CP + ch * WN + j * 32 + frow] = acc[i][j][r];
   });
 
-  // C layout of the 32x32 block: lane l holds column l % 32 and, in register
-  // r, row 8 * (r / 4) + 4 * (l / 32) + r % 4; the pair rows (even, odd) sit in
-  // registers r, r + 1 of the same lane.
-  const int rq = (lane >> 5) * 4;
-  auto for_my_half = [&](auto &&fn) __attribute__((always_inline)) {
-    // fn(i, j, r) for the even r of this wave's half (kh is wave-uniform)
-    static_for<0, NF / 2>([&](auto pc) __attribute__((always_inline)) {
-      constexpr int f = 2 * decltype(pc)::value;
-      constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
-      if (f / HF == kh) fn(std::integral_constant<int, i>{}, std::integral_constant<int, j>{},
-                          std::integral_constant<int, r>{});
-    });
-  };
   if constexpr (!TEXT) {
-    float bias[NB];
+    // thread -> fixed chunk c (4 columns) of GEMM row pairs q = item / CH
+    constexpr int CH = BN / 4;
+    constexpr int ITEMS = (BM / 2) * CH / 256;
+    static_assert(ITEMS >= 1 && (BM / 2) * CH % 256 == 0, "whole items per thread");
+    const int c = tid % CH;
+    const int nc = n0 + 4 * c;
+    floatx4 bias = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (hv.bias) {
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int n = n0 + ch * WN + j * 32 + frow;
-      bias[j] = (hv.bias && n < N) ? hv.bias[n] : 0.0f;
+      for (int e = 0; e < 4; ++e) bias[e] = (nc + e < N) ? hv.bias[nc + e] : 0.0f;
     }
-    // one instance per k half, so that every register index is a constant
-    auto epilogue = [&](auto khc) __attribute__((always_inline)) {
-      constexpr int KH = decltype(khc)::value;
-      static_for<0, HF / 2>([&](auto kc) __attribute__((always_inline)) {
-        constexpr int f = KH * HF + 2 * decltype(kc)::value;   // flat index, even r
-        constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
-        const int gl = i * 32 + (r >> 2) * 8 + rq + (r & 3);   // even GEMM row within the tile
-        const int g = m0 + gl;
-        const int n = n0 + ch * WN + j * 32 + frow;
-        const float4 pr = rowp[gl >> 1];
-        const float v0 = acc[i][j][r] + bias[j], v1 = acc[i][j][r + 1] + bias[j];
-        if (g < M && n < N) {
-          const int o0 = __float_as_int(pr.z), o1 = __float_as_int(pr.w);
-          if (o1 == -2) {
-            sv.scores[(size_t)o0 * N + n] = fmaf(pr.x, v0, (1.0f - pr.x) * v1) * pr.y;
-          } else {
-            if (o0 >= 0) sv.scores[(size_t)o0 * N + n] = v0 * pr.x;
-            if (o1 >= 0) sv.scores[(size_t)o1 * N + n] = v1 * pr.y;
-          }
-        }
-      });
+    wait_vmem_and_lds<0>();
+    __syncthreads();
+    const bool vec_ok = (N % 4 == 0) && (nc + 4 <= N);
+    auto put = [&](int out, const floatx4 &v) __attribute__((always_inline)) {
+      float *dst = sv.scores + (size_t)out * N + nc;
+      if (vec_ok) {
+        *reinterpret_cast<floatx4 *>(dst) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (nc + e < N) dst[e] = v[e];
+      }
     };
-    if (kh == 0) epilogue(std::integral_constant<int, 0>{});
-    else epilogue(std::integral_constant<int, 1>{});
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int q = (it * 256 + tid) / CH;
+      if (m0 + 2 * q >= M || nc >= N) continue;
+      const float *c0 = C + (2 * q) * CP + 4 * c;
+      const floatx4 v0 = *reinterpret_cast<const floatx4 *>(c0) +
+                         *reinterpret_cast<const floatx4 *>(c0 + BM * CP) + bias;
+      const floatx4 v1 = *reinterpret_cast<const floatx4 *>(c0 + CP) +
+                         *reinterpret_cast<const floatx4 *>(c0 + CP + BM * CP) + bias;
+      const float4 pr = rowp[q];
+      const int o0 = __float_as_int(pr.z), o1 = __float_as_int(pr.w);
+      if (o1 == -2) {
+        floatx4 s;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[e] = fmaf(pr.x, v0[e], (1.0f - pr.x) * v1[e]) * pr.y;
+        put(o0, s);
+      } else {
+        if (o0 >= 0) put(o0, v0 * pr.x);
+        if (o1 >= 0) put(o1, v1 * pr.y);
+      }
+    }
   } else {
-    static_assert(kTextPartCols == 32, "one 32-column block per text part");
-    for_my_half([&](auto ic, auto jc, auto rc) __attribute__((always_inline)) {
-      constexpr int i = decltype(ic)::value, j = decltype(jc)::value, r0 = decltype(rc)::value;
-      const int n = n0 + ch * WN + j * 32 + frow;
-      const int part = (n0 + ch * WN + j * 32) / kTextPartCols;
+    // thread -> (row, 32-column part): sequential scan, lowest id on ties
+    static_assert(kTextPartCols == 32 && BN % 32 == 0, "text parts are 32 columns");
+    constexpr int PPR = BN / 32;
+    __syncthreads();
+    for (int item = tid; item < BM * PPR; item += 256) {
+      const int row = item / PPR, p = item % PPR;
+      const int g = m0 + row;
+      const int part = (n0 + 32 * p) / kTextPartCols;
+      if (g >= M || part >= sv.text_parts) continue;
+      const float *c0 = C + row * CP + 32 * p;
+      float bv = -INFINITY;
+      int bi = INT32_MAX;
 #pragma unroll
-      for (int r = r0; r < r0 + 2; ++r) {
-        float bv = -INFINITY;
-        int bi = INT32_MAX;
-        if (n < N) {
-          bv = acc[i][j][r];
-          bi = n;
-        }
+      for (int x4 = 0; x4 < 8; ++x4) {
+        const floatx4 v = *reinterpret_cast<const floatx4 *>(c0 + 4 * x4) +
+                          *reinterpret_cast<const floatx4 *>(c0 + 4 * x4 + BM * CP);
 #pragma unroll
-        for (int off = 1; off < 32; off <<= 1) {
-          const float ov = __shfl_xor(bv, off);
-          const int oi = __shfl_xor(bi, off);
-          better(bv, bi, ov, oi);
-        }
-        const int g = m0 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
-        if (frow == 0 && g < M && part < sv.text_parts) {
-          sv.text_val[(size_t)g * sv.text_parts + part] = bv;
-          sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
+        for (int e = 0; e < 4; ++e) {
+          const int n = n0 + 32 * p + 4 * x4 + e;
+          if (n < N) better(bv, bi, v[e], n);
         }
       }
-    });
+      sv.text_val[(size_t)g * sv.text_parts + part] = bv;
+      sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
+    }
   }
 }
 
