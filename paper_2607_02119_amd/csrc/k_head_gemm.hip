@@ -79,164 +79,6 @@ __device__ inline void better(float &bv, int &bi, float v, int i) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA path.  256 threads = 4 waves in a 2x2 layout; tile BM x BN; the H
-// loop runs in 64-wide slices staged through LDS (double-buffered, one barrier
-// per slice).  Each wave owns a (BM/2) x (BN/2) sub-tile of 16x16 MFMA blocks
-// (v_mfma_f32_16x16x32_bf16: lane l holds A row l%16 / B column l%16 with 8
-// consecutive k; the 4 results of a lane are rows 4*(l/16)+0..3, column l%16).
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;  // padded LDS row (elements) against bank conflicts
-
-template <int BM, int BN, bool TEXT>
-__global__ __launch_bounds__(256) void head_gemm_bf16(HeadView hv, StepView sv) {
-  constexpr int MB = BM / 32;      // 16-row blocks per wave
-  constexpr int NB = BN / 32;      // 16-col blocks per wave
-  constexpr int ACH = BM * BK / 8 / 256;  // 16-byte chunks per thread (A tile)
-  constexpr int BCH = BN * BK / 8 / 256;  // (B tile)
-  static_assert(ACH >= 1 && BCH >= 1, "tile too small");
-
-  __shared__ __attribute__((aligned(16))) __bf16 As[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bs[2][BN * LDK];
-
-  if (!plan_ok(sv)) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-    return;
-  }
-  const int32_t *rows = sv.plan + kPlanHeader + (TEXT ? sv.Mg : 0);
-  const int M = TEXT ? sv.n_text : sv.Mg;
-  const int N = TEXT ? hv.V_text : hv.N;
-  const __bf16 *Wp = static_cast<const __bf16 *>(TEXT ? hv.W_text : hv.W);
-  const __bf16 *X = static_cast<const __bf16 *>(sv.hidden);
-  const int H = hv.H;
-
-  const int tiles_m = (M + BM - 1) / BM;
-  const int tile_m = blockIdx.x % tiles_m;
-  const int tile_n = blockIdx.x / tiles_m;
-  const int m0 = tile_m * BM, n0 = tile_n * BN;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  // global source pointers of this thread's chunks (nullptr: zero fill)
-  const __bf16 *asrc[ACH];
-  const __bf16 *bsrc[BCH];
-  int aoff[ACH], boff[BCH];
-#pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, col = (c & 7) * 8;
-    const int m = m0 + row;
-    asrc[i] = nullptr;
-    if (m < M) {
-      const int r = rows[m];
-      if (r >= 0 && r < sv.R) asrc[i] = X + (size_t)r * H + col;
-      else atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-    }
-    aoff[i] = row * LDK + col;
-  }
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, col = (c & 7) * 8;
-    const int n = n0 + row;
-    bsrc[i] = (n < N) ? Wp + (size_t)n * H + col : nullptr;
-    boff[i] = row * LDK + col;
-  }
-
-  u32x4 areg[ACH], breg[BCH];
-  auto load = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i)
-      areg[i] = asrc[i] ? *reinterpret_cast<const u32x4 *>(asrc[i] + kt * BK) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int i = 0; i < BCH; ++i)
-      breg[i] = bsrc[i] ? *reinterpret_cast<const u32x4 *>(bsrc[i] + kt * BK) : u32x4{0u, 0u, 0u, 0u};
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) *reinterpret_cast<u32x4 *>(&As[buf][aoff[i]]) = areg[i];
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) *reinterpret_cast<u32x4 *>(&Bs[buf][boff[i]]) = breg[i];
-  };
-
-  floatx4 acc[MB][NB];
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const int KT = H / BK;
-  load(0);
-  store(0);
-  __syncthreads();
-  const int frow = lane & 15, fk = (lane >> 4) * 8;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) load(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 a[MB], b[NB];
-#pragma unroll
-      for (int i = 0; i < MB; ++i)
-        a[i] = *reinterpret_cast<const bf16x8 *>(
-            &As[buf][(wm * (BM / 2) + i * 16 + frow) * LDK + ks * 32 + fk]);
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        b[j] = *reinterpret_cast<const bf16x8 *>(
-            &Bs[buf][(wn * (BN / 2) + j * 16 + frow) * LDK + ks * 32 + fk]);
-#pragma unroll
-      for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) store(buf ^ 1);
-    __syncthreads();
-  }
-
-  const int rq = (lane >> 4) * 4;  // first of the lane's 4 rows in a block
-  if constexpr (!TEXT) {
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int g = m0 + wm * (BM / 2) + i * 16 + rq;
-        const int n = n0 + wn * (BN / 2) + j * 16 + frow;
-        emit_audio(hv, sv, rows, g, acc[i][j][0], acc[i][j][1], n);
-        emit_audio(hv, sv, rows, g + 2, acc[i][j][2], acc[i][j][3], n);
-      }
-  } else {
-    // each wave's column half is two 32-column parts (blocks j = 0,1 and 2,3)
-    static_assert(NB % 2 == 0 && kTextPartCols == 32, "text parts are 32 columns");
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int jp = 0; jp < NB; jp += 2) {
-          float bv = -INFINITY;
-          int bi = INT32_MAX;
-#pragma unroll
-          for (int j = jp; j < jp + 2; ++j) {
-            const int n = n0 + wn * (BN / 2) + j * 16 + frow;
-            if (n < N) better(bv, bi, acc[i][j][q], n);
-          }
-#pragma unroll
-          for (int off = 1; off < 16; off <<= 1) {
-            const float ov = __shfl_xor(bv, off);
-            const int oi = __shfl_xor(bi, off);
-            better(bv, bi, ov, oi);
-          }
-          const int g = m0 + wm * (BM / 2) + i * 16 + rq + q;
-          const int part = (n0 + wn * (BN / 2) + jp * 16) / kTextPartCols;
-          if (frow == 0 && g < M && part < sv.text_parts) {
-            sv.text_val[(size_t)g * sv.text_parts + part] = bv;
-            sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
-          }
-        }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Weight-streaming path for up to 128 rows, staged with direct global->LDS
 // loads.  A workgroup owns all BM rows and BN columns.  Each k slice of SK = 64
 // (128 bytes of every weight and hidden row) is copied into one of S LDS
@@ -286,6 +128,129 @@ __device__ __forceinline__ void block_barrier_no_vmem_wait() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_barrier();
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Epilogue parameters of GEMM rows g0 (even) and g0 + 1: {w, 1/T, out, -2} for
+// a CFG pair (the Main row carries w and T), {1/T0, 1/T1, out0, out1} for solo
+// rows (out -1: no such row).
+__device__ inline float4 pair_params(const StepView &sv, const int32_t *rows, int g0) {
+  float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
+  if (g0 < 2 * sv.n_pairs) {
+    const int r = rows[g0];
+    if (r >= 0 && r < sv.R) {
+      const float T = sv.temperature[r];
+      pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
+                       __int_as_float(-2));
+    }
+    return pr;
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int g = g0 + h;
+    if (g < sv.Mg) {
+      const int r = rows[g];
+      if (r >= 0 && r < sv.R) {
+        const float T = sv.temperature[r];
+        const float it = T > 0.0f ? 1.0f / T : 1.0f;
+        const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
+        if (h == 0) {
+          pr.x = it;
+          pr.z = __int_as_float(out);
+        } else {
+          pr.y = it;
+          pr.w = __int_as_float(out);
+        }
+      }
+    }
+  }
+  return pr;
+}
+
+// Second phase of the LDS epilogue of a BM x BN tile whose sums sit in C
+// (pitch CP floats; NH = 2: two k-half arrays BM * CP apart, added here).
+// Audio: each thread owns a fixed 4-column chunk and walks row pairs, adds the
+// bias, applies the CFG merge (Eq. 1) and 1/T, and stores 16 bytes per output
+// row.  Text: each thread scans whole 32-column parts of rows and writes the
+// (max, lowest argmax) partials.  Starts with a workgroup barrier.
+template <int BM, int BN, int CP, bool TEXT, int NH>
+__device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const StepView &sv,
+                                                  const float *C, const float4 *rowp, int m0,
+                                                  int n0, int M, int N) {
+  const int tid = threadIdx.x;
+  auto sum4 = [&](const float *p) __attribute__((always_inline)) {
+    floatx4 v = *reinterpret_cast<const floatx4 *>(p);
+    if constexpr (NH == 2) v = v + *reinterpret_cast<const floatx4 *>(p + BM * CP);
+    return v;
+  };
+  if constexpr (!TEXT) {
+    constexpr int CH = BN / 4;
+    constexpr int ITEMS = (BM / 2) * CH / 256;
+    static_assert(ITEMS >= 1 && (BM / 2) * CH % 256 == 0, "whole items per thread");
+    const int c = tid % CH;
+    const int nc = n0 + 4 * c;
+    floatx4 bias = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (hv.bias) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bias[e] = (nc + e < N) ? hv.bias[nc + e] : 0.0f;
+    }
+    // no global load may stay pending among the stores below
+    wait_vmem_and_lds<0>();
+    __syncthreads();
+    const bool vec_ok = (N % 4 == 0) && (nc + 4 <= N);
+    auto put = [&](int out, const floatx4 &v) __attribute__((always_inline)) {
+      float *dst = sv.scores + (size_t)out * N + nc;
+      if (vec_ok) {
+        *reinterpret_cast<floatx4 *>(dst) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (nc + e < N) dst[e] = v[e];
+      }
+    };
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int q = (it * 256 + tid) / CH;
+      if (m0 + 2 * q >= M || nc >= N) continue;
+      const float *c0 = C + (2 * q) * CP + 4 * c;
+      const floatx4 v0 = sum4(c0) + bias;
+      const floatx4 v1 = sum4(c0 + CP) + bias;
+      const float4 pr = rowp[q];
+      const int o0 = __float_as_int(pr.z), o1 = __float_as_int(pr.w);
+      if (o1 == -2) {
+        floatx4 s;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[e] = fmaf(pr.x, v0[e], (1.0f - pr.x) * v1[e]) * pr.y;
+        put(o0, s);
+      } else {
+        if (o0 >= 0) put(o0, v0 * pr.x);
+        if (o1 >= 0) put(o1, v1 * pr.y);
+      }
+    }
+  } else {
+    static_assert(kTextPartCols == 32 && BN % 32 == 0, "text parts are 32 columns");
+    constexpr int PPR = BN / 32;
+    __syncthreads();
+    for (int item = tid; item < BM * PPR; item += 256) {
+      const int row = item / PPR, p = item % PPR;
+      const int g = m0 + row;
+      const int part = (n0 + 32 * p) / kTextPartCols;
+      if (g >= M || part >= sv.text_parts) continue;
+      const float *c0 = C + row * CP + 32 * p;
+      float bv = -INFINITY;
+      int bi = INT32_MAX;
+#pragma unroll
+      for (int x4 = 0; x4 < 8; ++x4) {
+        const floatx4 v = sum4(c0 + 4 * x4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int n = n0 + 32 * p + 4 * x4 + e;
+          if (n < N) better(bv, bi, v[e], n);
+        }
+      }
+      sv.text_val[(size_t)g * sv.text_parts + part] = bv;
+      sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
+    }
+  }
 }
 
 template <int BM, int BN, bool TEXT>
@@ -409,39 +374,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     });
     const int q2 = tid - 128;
-    if (!TEXT && q2 < BM / 2) {
-      const int g0 = m0 + 2 * q2;
-      float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
-      if (g0 < 2 * sv.n_pairs) {
-        const int r = rows[g0];              // the pair's Main row carries w and T
-        if (r >= 0 && r < sv.R) {
-          const float T = sv.temperature[r];
-          pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
-                           __int_as_float(-2));
-        }
-      } else {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int g = g0 + h;
-          if (g < sv.Mg) {
-            const int r = rows[g];
-            if (r >= 0 && r < sv.R) {
-              const float T = sv.temperature[r];
-              const float it = T > 0.0f ? 1.0f / T : 1.0f;
-              const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
-              if (h == 0) {
-                pr.x = it;
-                pr.z = __int_as_float(out);
-              } else {
-                pr.y = it;
-                pr.w = __int_as_float(out);
-              }
-            }
-          }
-        }
-      }
-      rowp[q2] = pr;
-    }
+    if (!TEXT && q2 < BM / 2) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
     wait_vmem_and_lds<0>();
 #pragma unroll
     for (int st = 0; st < SA - 1; ++st) issue_a(st);
@@ -519,79 +452,250 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     C[(kh * BM + row) * CP + ch * WN + j * 32 + frow] = acc[i][j][r];
   });
 
-  if constexpr (!TEXT) {
-    // thread -> fixed chunk c (4 columns) of GEMM row pairs q = item / CH
-    constexpr int CH = BN / 4;
-    constexpr int ITEMS = (BM / 2) * CH / 256;
-    static_assert(ITEMS >= 1 && (BM / 2) * CH % 256 == 0, "whole items per thread");
-    const int c = tid % CH;
-    const int nc = n0 + 4 * c;
-    floatx4 bias = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (hv.bias) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) bias[e] = (nc + e < N) ? hv.bias[nc + e] : 0.0f;
-    }
-    wait_vmem_and_lds<0>();
-    __syncthreads();
-    const bool vec_ok = (N % 4 == 0) && (nc + 4 <= N);
-    auto put = [&](int out, const floatx4 &v) __attribute__((always_inline)) {
-      float *dst = sv.scores + (size_t)out * N + nc;
-      if (vec_ok) {
-        *reinterpret_cast<floatx4 *>(dst) = v;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (nc + e < N) dst[e] = v[e];
+  epilogue_from_lds<BM, BN, CP, TEXT, 2>(hv, sv, C, rowp, m0, n0, M, N);
+}
+
+// ---------------------------------------------------------------------------
+// MFMA-regime path for more than 128 GEMM rows (bf16, H a multiple of 32).
+// A workgroup owns a 256 x 128 output tile.  The waves split it by row half
+// (wm = wave & 1) and k half (kh = wave >> 1): each wave accumulates a
+// 128 x 128 block (4 x 4 blocks of v_mfma_f32_32x32x16_bf16, 256 accumulator
+// registers) over its 16 k of every 32-k slice, so each MFMA costs half a
+// fragment of LDS reads.  Slices are copied global->LDS like the streaming
+// path: waves 0-1 copy weight slices into a deep ring (the weights come from
+// HBM, once per XCD), waves 2-3 copy hidden-state slices into a shorter one
+// (they are re-read from L2).  A slice row is 64 bytes, 4 chunks of 16 B;
+// chunk c of row r is stored at position c ^ ((r >> 2) & 3), so the 16 rows
+// of a 16-lane fragment read group hit all 64 banks once.
+//
+// Tile order is XCD-aware: workgroups are dealt to the 8 XCDs in turn, so the
+// grid index is remapped to give each XCD a contiguous run of tiles, in which
+// the row tiles of a column tile are neighbours and run at the same time:
+// they share that column's weights through the XCD's L2.
+constexpr int kMfmaBM = 256, kMfmaBN = 128, kMfmaSK = 32;
+constexpr int kMfmaSA = 5, kMfmaSB = 8;
+
+template <bool TEXT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void head_gemm_mfma(
+    HeadView hv, StepView sv) {
+  constexpr int BM = kMfmaBM, BN = kMfmaBN, SK = kMfmaSK;
+  constexpr int SA = kMfmaSA, SB = kMfmaSB;
+  constexpr int ROWB = SK * 2;                       // 64 bytes per row and slice
+  constexpr int AST = BM * ROWB, BST = BN * ROWB;    // 16 KiB, 8 KiB per stage
+  constexpr int AIA = AST / 1024 / 2, BIB = BST / 1024 / 2;  // copies per wave per slice
+  constexpr int MB = 4, NB = 4;                      // 32x32 blocks per wave
+  static_assert((SA - 1) * AIA < 64 && (SB - 1) * BIB < 64, "vmcnt range");
+  // both copy roles keep the same number of copies in flight in the loop, so
+  // that its one wait needs no branch (a branch makes the compiler's own
+  // LDS-read waits conservative)
+  constexpr int kLoopVm = (SA - 2) * AIA;
+  static_assert((SB - 2) * BIB == kLoopVm, "equal in-flight copy counts");
+  static_assert(MB * NB == 16 && AIA == 8 && BIB == 4, "copy slots of the slice schedule");
+  constexpr int CP = BN + 4;                         // epilogue row pitch (floats)
+  static_assert(BM * CP * 4 <= SA * AST + SB * BST, "epilogue tile fits the rings");
+
+  __shared__ __attribute__((aligned(1024))) char lds[SA * AST + SB * BST];
+  char *const aring = lds;
+  char *const bring = lds + SA * AST;
+  __shared__ float4 rowp[BM / 2];
+
+  const int32_t *rows = sv.plan + kPlanHeader + (TEXT ? sv.Mg : 0);
+  const int M = TEXT ? sv.n_text : sv.Mg;
+  const int N = TEXT ? hv.V_text : hv.N;
+  const __bf16 *Wp = static_cast<const __bf16 *>(TEXT ? hv.W_text : hv.W);
+  const __bf16 *X = static_cast<const __bf16 *>(sv.hidden);
+  const int H = hv.H;
+  const int NST = H / SK;
+
+  const int tiles_m = (M + BM - 1) / BM;
+  int bx = blockIdx.x;
+  if (gridDim.x % 8 == 0) bx = (bx % 8) * (gridDim.x / 8) + bx / 8;
+  const int tile_m = bx % tiles_m, tile_n = bx / tiles_m;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 1, kh = wave >> 1;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const bool b_copier = wave_s < 2;
+
+  // the row tiles of one column tile walk k in the same order (they share the
+  // weights in L2); different column tiles start at different k
+  const int kskew = (int)(((unsigned)tile_n * 7u) % (unsigned)NST);
+  const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)aring;
+  const uint32_t bbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)bring;
+  // one copy instruction: 16 rows x 4 chunks; lane i -> row i / 4, position i % 4
+  const int seg_r = lane >> 2, seg_p = lane & 3;
+  constexpr int QN = AIA > BIB ? AIA : BIB;
+  const __bf16 *src[QN];
+  auto issue_b = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = bbase + (uint32_t)((st % SB) * BST);
+    static_for<0, BIB>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)((wave_s * BIB + q) * 1024));
+    });
+  };
+  auto issue_a = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = abase + (uint32_t)((st % SA) * AST);
+    static_for<0, AIA>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+    });
+  };
+
+  wait_vmem_and_lds<0>();
+  if (b_copier) {
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < BIB) {
+        const int r = (wave_s * BIB + q) * 16 + seg_r;
+        const int n = min(n0 + r, N - 1);
+        src[q] = Wp + (size_t)n * H + ((seg_p ^ ((r >> 2) & 3)) * 8);
       }
-    };
+    });
 #pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int q = (it * 256 + tid) / CH;
-      if (m0 + 2 * q >= M || nc >= N) continue;
-      const float *c0 = C + (2 * q) * CP + 4 * c;
-      const floatx4 v0 = *reinterpret_cast<const floatx4 *>(c0) +
-                         *reinterpret_cast<const floatx4 *>(c0 + BM * CP) + bias;
-      const floatx4 v1 = *reinterpret_cast<const floatx4 *>(c0 + CP) +
-                         *reinterpret_cast<const floatx4 *>(c0 + CP + BM * CP) + bias;
-      const float4 pr = rowp[q];
-      const int o0 = __float_as_int(pr.z), o1 = __float_as_int(pr.w);
-      if (o1 == -2) {
-        floatx4 s;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) s[e] = fmaf(pr.x, v0[e], (1.0f - pr.x) * v1[e]) * pr.y;
-        put(o0, s);
-      } else {
-        if (o0 >= 0) put(o0, v0 * pr.x);
-        if (o1 >= 0) put(o1, v1 * pr.y);
-      }
-    }
-  } else {
-    // thread -> (row, 32-column part): sequential scan, lowest id on ties
-    static_assert(kTextPartCols == 32 && BN % 32 == 0, "text parts are 32 columns");
-    constexpr int PPR = BN / 32;
-    __syncthreads();
-    for (int item = tid; item < BM * PPR; item += 256) {
-      const int row = item / PPR, p = item % PPR;
-      const int g = m0 + row;
-      const int part = (n0 + 32 * p) / kTextPartCols;
-      if (g >= M || part >= sv.text_parts) continue;
-      const float *c0 = C + row * CP + 32 * p;
-      float bv = -INFINITY;
-      int bi = INT32_MAX;
-#pragma unroll
-      for (int x4 = 0; x4 < 8; ++x4) {
-        const floatx4 v = *reinterpret_cast<const floatx4 *>(c0 + 4 * x4) +
-                          *reinterpret_cast<const floatx4 *>(c0 + 4 * x4 + BM * CP);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int n = n0 + 32 * p + 4 * x4 + e;
-          if (n < N) better(bv, bi, v[e], n);
-        }
-      }
-      sv.text_val[(size_t)g * sv.text_parts + part] = bv;
-      sv.text_idx[(size_t)g * sv.text_parts + part] = bi;
-    }
+    for (int st = 0; st < SB; ++st) issue_b(st);
   }
+
+  if (!plan_ok(sv)) {
+    wait_vmem_and_lds<0>();  // no copy may still be landing in this workgroup's LDS
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    return;
+  }
+
+  if (!b_copier) {
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < AIA) {
+        const int r = ((wave_s - 2) * AIA + q) * 16 + seg_r;
+        int pr = rows[min(m0 + r, M - 1)];
+        if (pr < 0 || pr >= sv.R) {
+          atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+          pr = 0;
+        }
+        src[q] = X + (size_t)pr * H + ((seg_p ^ ((r >> 2) & 3)) * 8);
+      }
+    });
+    const int q2 = tid - 128;
+    if (!TEXT) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
+    wait_vmem_and_lds<0>();
+#pragma unroll
+    for (int st = 0; st < SA; ++st) issue_a(st);
+  }
+
+  floatx16 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // fragment offsets: lane l holds row (column) l % 32 and chunk 2 kh + l / 32
+  const int frow = lane & 31;
+  const int fch = 2 * kh + (lane >> 5);
+  int aoff[MB], boff[NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i) {
+    const int r = wm * 128 + i * 32 + frow;
+    aoff[i] = r * ROWB + ((fch ^ ((r >> 2) & 3)) * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int r = j * 32 + frow;
+    boff[j] = r * ROWB + ((fch ^ ((r >> 2) & 3)) * 16);
+  }
+
+  // Software pipeline: the fragments of slice st + 1 are read from LDS while
+  // the MFMAs of slice st run on the registers read one iteration earlier.
+  // At the top of iteration st every wave waits for its copies of slice st + 1
+  // and for its own fragment reads of slice st; the barrier extends both to the
+  // workgroup, so the stage of slice st is free for slice st + S (A: S = SA,
+  // B: S = SB), which is issued right after it.  Slices past the end re-load
+  // the last one (clamped), so every iteration issues the same count.
+  bf16x8 fa0[MB], fb0[NB], fa1[MB], fb1[NB];
+  auto read_frags = [&](int st, bf16x8 (&fa)[MB], bf16x8 (&fb)[NB])
+      __attribute__((always_inline)) {
+    const char *asb = aring + (st % SA) * AST;
+    const char *bsb = bring + (st % SB) * BST;
+#pragma unroll
+    for (int i = 0; i < MB; ++i) fa[i] = *reinterpret_cast<const bf16x8 *>(asb + aoff[i]);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) fb[j] = *reinterpret_cast<const bf16x8 *>(bsb + boff[j]);
+  };
+  // One slice: its 16 MFMAs, with the 8 fragment reads of the next slice and
+  // this wave's copies (A: 8 per slice, B: 4) spread between them, so that the
+  // MFMA pipe, the LDS and the load path (the per-CU limit here: a slice moves
+  // 24 KiB) all work at once instead of in turn.
+  auto step = [&](int st, bf16x8 (&fa)[MB], bf16x8 (&fb)[NB], bf16x8 (&na)[MB],
+                  bf16x8 (&nb)[NB]) __attribute__((always_inline)) {
+    wait_vmem_and_lds<kLoopVm>();
+    block_barrier_no_vmem_wait();
+    const int cst = st + (b_copier ? SB : SA);   // slice this wave copies now
+    int ks = min(cst, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t csb = b_copier ? bbase + (uint32_t)((cst % SB) * BST)
+                                  : abase + (uint32_t)((cst % SA) * AST);
+    const int st1 = st + 1;   // past the end: a clamped slice, never used
+    const char *asb = aring + (st1 % SA) * AST;
+    const char *bsb = bring + (st1 % SB) * BST;
+    static_for<0, MB * NB>([&](auto mc) __attribute__((always_inline)) {
+      constexpr int m = decltype(mc)::value;
+      constexpr int i = m / NB, j = m % NB;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      if constexpr (m < MB) na[m] = *reinterpret_cast<const bf16x8 *>(asb + aoff[m]);
+      else if constexpr (m < MB + NB) nb[m - MB] = *reinterpret_cast<const bf16x8 *>(bsb + boff[m - MB]);
+      if constexpr (m % 2 == 1) {
+        constexpr int q = m / 2;           // A copies 0..7 after the odd MFMAs
+        if (!b_copier) lds_copy16(src[q] + ks * SK, csb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+      }
+      if constexpr (m % 4 == 3) {
+        constexpr int q = m / 4;           // B copies 0..3 after every fourth
+        if (b_copier) lds_copy16(src[q] + ks * SK, csb + (uint32_t)((wave_s * BIB + q) * 1024));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+  // slice 0: landed (all but SA - 1 / SB - 1 newer slices), then its fragments
+  if (b_copier) wait_vmem_and_lds<(SB - 1) * BIB>();
+  else wait_vmem_and_lds<(SA - 1) * AIA>();
+  block_barrier_no_vmem_wait();
+  read_frags(0, fa0, fb0);
+  for (int st = 0; st < NST; st += 2) {   // NST is even (H % 64 == 0)
+    step(st, fa0, fb0, fa1, fb1);
+    step(st + 1, fa1, fb1, fa0, fb0);
+  }
+  wait_vmem_and_lds<0>();
+  __syncthreads();
+
+  // Epilogue through LDS: the k-half-1 waves store their sums in C[row][col],
+  // the k-half-0 waves add theirs in place (a two-term sum: order-free), then
+  // every thread applies the fused epilogue to 16-byte column chunks.
+  float *C = reinterpret_cast<float *>(lds);
+  // element (i, j, r) of this lane sits at Cl + a compile-time offset
+  float *Cl = C + (wm * 128 + (lane >> 5) * 4) * CP + frow;
+  if (kh == 1) {
+    static_for<0, MB * NB * 16>([&](auto fc) __attribute__((always_inline)) {
+      constexpr int f = decltype(fc)::value;
+      constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+      constexpr int off = (i * 32 + (r >> 2) * 8 + (r & 3)) * CP + j * 32;
+      Cl[off] = acc[i][j][r];
+    });
+  }
+  __syncthreads();
+  if (kh == 0) {
+    static_for<0, MB * NB * 16>([&](auto fc) __attribute__((always_inline)) {
+      constexpr int f = decltype(fc)::value;
+      constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+      constexpr int off = (i * 32 + (r >> 2) * 8 + (r & 3)) * CP + j * 32;
+      Cl[off] = acc[i][j][r] + Cl[off];
+    });
+  }
+  epilogue_from_lds<BM, BN, CP, TEXT, 1>(hv, sv, C, rowp, m0, n0, M, N);
 }
 
 // fp32 path (plain FMA, ascending h).  256 threads: 64 columns x 4 row lanes;
@@ -653,10 +757,10 @@ __global__ __launch_bounds__(256) void head_gemm_f32(HeadView hv, StepView sv) {
   }
 }
 
-template <int BM, int BN, bool TEXT>
-hipError_t launch_bf16(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
-  const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-  hipLaunchKernelGGL((head_gemm_bf16<BM, BN, TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
+template <bool TEXT>
+hipError_t launch_mfma(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  const int tm = (M + kMfmaBM - 1) / kMfmaBM, tn = (N + kMfmaBN - 1) / kMfmaBN;
+  hipLaunchKernelGGL((head_gemm_mfma<TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
   return hipGetLastError();
 }
 
@@ -695,11 +799,11 @@ hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t 
   }
   if (sv.Mg > 0) {
     if (sv.Mg <= 128) e = launch_skinny<false>(hv, sv, sv.Mg, hv.N, st);
-    else e = launch_bf16<128, 128, false>(hv, sv, sv.Mg, hv.N, st);
+    else e = launch_mfma<false>(hv, sv, sv.Mg, hv.N, st);
   }
   if (e == hipSuccess && sv.n_text > 0) {
     if (sv.n_text <= 128) e = launch_skinny<true>(hv, sv, sv.n_text, hv.V_text, st);
-    else e = launch_bf16<128, 128, true>(hv, sv, sv.n_text, hv.V_text, st);
+    else e = launch_mfma<true>(hv, sv, sv.n_text, hv.V_text, st);
   }
   return e;
 }

@@ -14,14 +14,23 @@
 //   * the token goes to the Main row, to its Companion (Sec. 2.4) and to the
 //     request's frame grid cell [k][f].
 //
-// Selection is a radix select over order-preserving 32-bit keys of the fp32
-// scores (8-bit digits from the top, histograms in LDS).  Top-k histograms
-// count elements and stop as soon as the bucket holding the cut is taken whole;
-// top-p histograms add fixed-point masses exp(s - max) * 2^48 (fp32 exp,
-// converted exactly) as 64-bit integers, so the sums are exact and independent
-// of the order of the adds.
-// Three rotating histogram buffers need one barrier per digit pass: every wave
-// scans the whole histogram itself, so no result has to be broadcast.
+// Layout: thread tid owns groups g = q * 256 + tid of four consecutive ids
+// 4g .. 4g + 3 (one 16-byte load each), so that one Philox block serves a whole
+// group from registers.
+//
+// Selection.  Every score s falls in a bin b = floor(16 (max - s)) (bins of
+// width 1/16 below the maximum, the last one open-ended); the bin index is
+// monotone in s, so a cut between bins is a cut in the (score desc, id asc)
+// order.  One histogram pass (counts for top-k, masses for top-p) finds the bin
+// holding the cut; only the few elements of that bin are then ranked exactly
+// against each other.  Top-p masses are fixed-point exp(s - max) * 2^48 (fp32
+// exp, converted exactly) summed as 64-bit integers: exact and independent of
+// the order of the adds.  Inputs whose cut bin is crowded (heavy ties, or a cut
+// far below the maximum) take a radix select over order-preserving 32-bit keys
+// instead; both give the same kept set.
+//
+// Wave reductions and scans use DPP lane moves (row shifts and row broadcasts)
+// rather than LDS permutes.
 #include "mcd_internal.h"
 
 namespace mcd {
@@ -30,11 +39,18 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
+constexpr int kBins = 512;          // bins of width 1/16 below the maximum, plus one open bin
+constexpr float kBinScale = 16.0f;
+constexpr int kCap = 256;           // largest cut bin ranked directly
 
 __device__ inline uint32_t order_key(float x) {
   if (x == 0.0f) x = 0.0f;  // -0 and +0 compare equal
   const uint32_t u = __float_as_uint(x);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ inline float key_to_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
 __device__ inline bool plan_ok(const StepView &sv) {
@@ -43,23 +59,8 @@ __device__ inline bool plan_ok(const StepView &sv) {
          p[kPlanSolo] == sv.n_solo && p[kPlanText] == sv.n_text;
 }
 
-template <int EPL>
-struct Smem {
-  unsigned long long hist[3][256];   // rotating digit histograms (counts or masses)
-  unsigned long long r64[2][kWaves];  // block reductions (double-buffered)
-  double rf[2][kWaves];
-  int ri[2][kWaves];
-  uint32_t cnt[EPL * kWaves];         // tie counts per (element slot, wave)
-  uint32_t kept[(EPL * kThreads + 31) / 32];  // kept-id bitmask
-};
-
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
 __device__ inline int wave_id() { return threadIdx.x / kWave; }
-
-__device__ inline uint64_t lanemask_lt() {
-  const int lane = lane_id();
-  return lane ? (~0ull >> (64 - lane)) : 0ull;
-}
 
 template <typename T>
 __device__ inline void keep_better(T &bv, int &bi, T v, int i) {
@@ -69,53 +70,197 @@ __device__ inline void keep_better(T &bv, int &bi, T v, int i) {
   }
 }
 
-// Block reductions; `slot` alternates between consecutive calls so that one
-// barrier suffices (the buffer written now was last read two calls ago).
-template <int EPL>
-__device__ inline uint64_t block_sum_u64(uint64_t x, Smem<EPL> &sm, int slot) {
+// ---- wave primitives (DPP) -------------------------------------------------
+// Lane move with an identity for lanes whose source lies outside the row (or
+// rows left out by the row mask).
+template <int CTRL, int ROWMASK = 0xF>
+__device__ __forceinline__ uint32_t dpp(uint32_t identity, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)v, CTRL, ROWMASK, 0xF, false);
+}
+constexpr int kShr1 = 0x111, kShr2 = 0x112, kShr4 = 0x114, kShr8 = 0x118;
+constexpr int kBcast15 = 0x142, kBcast31 = 0x143;
+
+// Inclusive scan over the 64 lanes: shifts by 1, 2, 4, 8 within 16-lane rows,
+// then the last lane of row 0 (2) into row 1 (3), and lane 31 into rows 2, 3.
+template <class Combine>
+__device__ __forceinline__ void wave_scan(Combine &&step) {
+  step(std::integral_constant<int, kShr1>{}, std::integral_constant<int, 0xF>{});
+  step(std::integral_constant<int, kShr2>{}, std::integral_constant<int, 0xF>{});
+  step(std::integral_constant<int, kShr4>{}, std::integral_constant<int, 0xF>{});
+  step(std::integral_constant<int, kShr8>{}, std::integral_constant<int, 0xF>{});
+  step(std::integral_constant<int, kBcast15>{}, std::integral_constant<int, 0xA>{});
+  step(std::integral_constant<int, kBcast31>{}, std::integral_constant<int, 0xC>{});
+}
+
+__device__ __forceinline__ uint32_t wave_incl_add_u32(uint32_t x) {
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    x += dpp<decltype(c)::value, decltype(m)::value>(0u, x);
+  });
+  return x;
+}
+
+__device__ __forceinline__ uint64_t wave_incl_add_u64(uint64_t x) {
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+    const uint32_t lo = dpp<C, RM>(0u, (uint32_t)x), hi = dpp<C, RM>(0u, (uint32_t)(x >> 32));
+    x += ((uint64_t)hi << 32) | lo;
+  });
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    const uint32_t o = dpp<decltype(c)::value, decltype(m)::value>(0u, x);
+    x = o > x ? o : x;
+  });
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    const uint32_t o = dpp<decltype(c)::value, decltype(m)::value>(0xFFFFFFFFu, x);
+    x = o < x ? o : x;
+  });
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// (value desc, id asc) best over the wave, as seen by every lane.
+__device__ __forceinline__ void wave_argmax_f32(float &bv, int &bi) {
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+    const float ov = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(bv)));
+    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)bi);
+    keep_better(bv, bi, ov, oi);
+  });
+  bv = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(bv), 63));
+  bi = __builtin_amdgcn_readlane(bi, 63);
+}
+
+__device__ __forceinline__ void wave_argmax_f64(double &bv, int &bi) {
+  const uint64_t ninf = (uint64_t)__double_as_longlong(-INFINITY);
+  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(c)::value, RM = decltype(m)::value;
+    const uint64_t b = (uint64_t)__double_as_longlong(bv);
+    const uint32_t lo = dpp<C, RM>((uint32_t)ninf, (uint32_t)b);
+    const uint32_t hi = dpp<C, RM>((uint32_t)(ninf >> 32), (uint32_t)(b >> 32));
+    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)bi);
+    keep_better(bv, bi, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oi);
+  });
+  bv = __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(bv), 63));
+  bi = __builtin_amdgcn_readlane(bi, 63);
+}
+
+// ---- workgroup shared memory and reductions ----------------------------------
+template <int GPT>
+struct Smem {
+  uint32_t cnt[kBins + 1];               // top-k bin counts
+  unsigned long long mh[kBins + 1];      // top-p bin masses
+  // elements of the cut bin, and their exact ranks
+  float lv[kCap];
+  int li[kCap];
+  unsigned long long lm[kCap];
+  int lr[kCap];
+  unsigned long long lsm[kCap];          // masses in rank order
+  uint32_t lcount;
+  // block reductions (two slots, alternating, one barrier each)
+  uint32_t ru[2][kWaves];
+  unsigned long long r64[2][kWaves];
+  double rd[2][kWaves];
+  int ri[2][kWaves];
+  // radix select (fallback)
+  unsigned long long hist[3][256];
+};
+
+template <int GPT>
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t x, Smem<GPT> &sm, int &slot) {
+  x = wave_max_u32(x);
+  if (lane_id() == 0) sm.ru[slot][wave_id()] = x;
+  __syncthreads();
+  uint32_t r = 0;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  for (int w = 0; w < kWaves; ++w) r = sm.ru[slot][w] > r ? sm.ru[slot][w] : r;
+  slot ^= 1;
+  return r;
+}
+
+template <int GPT>
+__device__ __forceinline__ uint32_t block_min_u32(uint32_t x, Smem<GPT> &sm, int &slot) {
+  x = wave_min_u32(x);
+  if (lane_id() == 0) sm.ru[slot][wave_id()] = x;
+  __syncthreads();
+  uint32_t r = 0xFFFFFFFFu;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) r = sm.ru[slot][w] < r ? sm.ru[slot][w] : r;
+  slot ^= 1;
+  return r;
+}
+
+template <int GPT>
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, Smem<GPT> &sm, int &slot) {
+  x = readlane_u64(wave_incl_add_u64(x), 63);
   if (lane_id() == 0) sm.r64[slot][wave_id()] = x;
   __syncthreads();
   uint64_t r = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) r += sm.r64[slot][w];
+  slot ^= 1;
   return r;
 }
 
-template <int EPL>
-__device__ inline uint64_t block_max_u64(uint64_t x, Smem<EPL> &sm, int slot) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t o = __shfl_xor(x, off);
-    x = o > x ? o : x;
-  }
-  if (lane_id() == 0) sm.r64[slot][wave_id()] = x;
+// exclusive prefix of x over the threads in id order, and the block total
+template <int GPT>
+__device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t &total,
+                                                        Smem<GPT> &sm, int &slot) {
+  const uint32_t incl = wave_incl_add_u32(x);
+  if (lane_id() == 63) sm.ru[slot][wave_id()] = incl;
   __syncthreads();
-  uint64_t r = 0;
+  uint32_t before = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = sm.r64[slot][w] > r ? sm.r64[slot][w] : r;
-  return r;
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = sm.ru[slot][w];
+    if (w < wave_id()) before += c;
+    tot += c;
+  }
+  slot ^= 1;
+  total = tot;
+  return before + incl - x;
 }
 
-// (value desc, id asc) maximum over the block; every thread gets the id.
-template <typename T, int EPL>
-__device__ inline int block_argmax(T bv, int bi, Smem<EPL> &sm, int slot) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const T ov = __shfl_xor(bv, off);
-    const int oi = __shfl_xor(bi, off);
-    keep_better(bv, bi, ov, oi);
-  }
+template <int GPT>
+__device__ __forceinline__ int block_argmax_f32(float bv, int bi, Smem<GPT> &sm, int &slot) {
+  wave_argmax_f32(bv, bi);
   if (lane_id() == 0) {
-    sm.rf[slot][wave_id()] = (double)bv;
+    sm.rd[slot][wave_id()] = (double)bv;
     sm.ri[slot][wave_id()] = bi;
   }
   __syncthreads();
-  double rv = sm.rf[slot][0];
+  double rv = sm.rd[slot][0];
   int ri = sm.ri[slot][0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rf[slot][w], sm.ri[slot][w]);
+  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
+  slot ^= 1;
+  return ri;
+}
+
+template <int GPT>
+__device__ __forceinline__ int block_argmax_f64(double bv, int bi, Smem<GPT> &sm, int &slot) {
+  wave_argmax_f64(bv, bi);
+  if (lane_id() == 0) {
+    sm.rd[slot][wave_id()] = bv;
+    sm.ri[slot][wave_id()] = bi;
+  }
+  __syncthreads();
+  double rv = sm.rd[slot][0];
+  int ri = sm.ri[slot][0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
+  slot ^= 1;
   return ri;
 }
 
@@ -153,7 +298,7 @@ __device__ inline float gumbel_from_word(uint64_t x) {
   return -logf(-logf(u));
 }
 
-// ---- radix select ------------------------------------------------------------
+// ---- radix select (fallback) -----------------------------------------------
 // Cut of "take `target` units from the top" among the active elements (units:
 // 1 per element, or its fixed-point mass).  Result: keep every active element
 // with key >= lo; when `exact`, lo is a single key kappa whose ties are kept
@@ -165,13 +310,13 @@ struct Cut {
   bool all;        // target not reached: keep every active element
 };
 
-// Element i of thread tid is id e = i*256 + tid.  `pass` counts the digit
-// passes done so far in this vector and selects the rotating buffers; the
-// buffers pass % 3 and (pass + 1) % 3 must be zero on entry, and the two after
-// the last one used are zero again on exit.
-template <int EPL, bool MASS>
-__device__ Cut radix_select(const float (&x)[EPL], uint32_t active, const uint64_t *mass,
-                            uint64_t target, Smem<EPL> &sm, int &pass) {
+// `pass` counts the digit passes done so far in this vector and selects the
+// rotating buffers; the buffers pass % 3 and (pass + 1) % 3 must be zero on
+// entry, and the two after the last one used are zero again on exit.
+template <int GPT, bool MASS>
+__device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t active, const uint64_t *mass,
+                            uint64_t target, Smem<GPT> &sm, int &pass) {
+  constexpr int EPL = 4 * GPT;
   const int tid = threadIdx.x, lane = lane_id();
   uint32_t prefix = 0, pmask = 0;
   uint64_t rem = target;
@@ -193,12 +338,7 @@ __device__ Cut radix_select(const float (&x)[EPL], uint32_t active, const uint64
       v[j] = h[255 - 4 * lane - j];
       lsum += v[j];
     }
-    uint64_t incl = lsum;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const uint64_t o = __shfl_up(incl, off);
-      if (lane >= off) incl += o;
-    }
+    const uint64_t incl = wave_incl_add_u64(lsum);
     const uint64_t excl = incl - lsum;
     // clear the buffer of the pass after next (its last readers passed the barrier above)
     sm.hist[(pass + 2) % 3][tid] = 0;
@@ -206,24 +346,19 @@ __device__ Cut radix_select(const float (&x)[EPL], uint32_t active, const uint64
     const uint64_t bal = __ballot(excl < rem && incl >= rem);
     if (bal == 0) return Cut{0u, false, 0, true};
     const int src = __ffsll((long long)bal) - 1;
+    uint64_t cum = readlane_u64(excl, src);
     int dsel = 0;
-    uint64_t above = 0, inbucket = 0;
-    if (lane == src) {
-      uint64_t cum = excl;
+    uint64_t above = cum, inbucket = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (cum + v[j] >= rem) {
-          dsel = 255 - 4 * lane - j;
-          above = cum;
-          inbucket = v[j];
-          break;
-        }
-        cum += v[j];
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t vj = readlane_u64(v[j], src);
+      if (inbucket == 0 && cum + vj >= rem) {
+        dsel = 255 - 4 * src - j;
+        above = cum;
+        inbucket = vj;
       }
+      cum += vj;
     }
-    dsel = __shfl(dsel, src);
-    above = __shfl(above, src);
-    inbucket = __shfl(inbucket, src);
     rem -= above;
     prefix |= (uint32_t)dsel << shift;
     pmask |= 255u << shift;
@@ -236,10 +371,12 @@ __device__ Cut radix_select(const float (&x)[EPL], uint32_t active, const uint64
 }
 
 // Apply a cut to the active set.  For an exact cut with fewer than all of the
-// ties at kappa wanted, the `need_n` lowest ids among the ties are kept.
-template <int EPL>
-__device__ uint32_t apply_cut(const float (&x)[EPL], uint32_t active, const Cut &c,
-                              uint64_t need_n, Smem<EPL> &sm, int &slot) {
+// ties at kappa wanted, the `need_n` lowest ids among the ties are kept (id of
+// slot 4q + j of thread tid: 4 (q * 256 + tid) + j).
+template <int GPT>
+__device__ __forceinline__ uint32_t apply_cut(const float (&x)[4 * GPT], uint32_t active, const Cut &c,
+                              uint64_t need_n, Smem<GPT> &sm, int &slot) {
+  constexpr int EPL = 4 * GPT;
   if (c.all) return active;
   uint32_t keep = 0, ties = 0;
 #pragma unroll
@@ -250,147 +387,348 @@ __device__ uint32_t apply_cut(const float (&x)[EPL], uint32_t active, const Cut 
     if (act && c.exact && key == c.lo) ties |= 1u << i;
   }
   if (!c.exact) return keep;
-  const uint64_t total = block_sum_u64((uint64_t)__popc(ties), sm, slot);
-  slot ^= 1;
-  if (need_n >= total) return keep | ties;
-  // rare: rank the ties by id (e = i*256 + tid)
-  const int lane = lane_id(), wave = wave_id();
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const uint64_t b = __ballot((ties >> i) & 1);
-    if (lane == 0) sm.cnt[i * kWaves + wave] = __popcll(b);
-  }
-  __syncthreads();
   uint64_t base = 0;
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const uint64_t b = __ballot((ties >> i) & 1);
-    uint64_t before = 0, tot = 0;
+  for (int q = 0; q < GPT; ++q) {
+    const uint32_t tq = (ties >> (4 * q)) & 0xFu;
+    uint32_t total;
+    const uint32_t before = block_excl_scan_u32((uint32_t)__popc(tq), total, sm, slot);
+    uint64_t rank = base + before;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const uint32_t cw = sm.cnt[i * kWaves + w];
-      if (w < wave) before += cw;
-      tot += cw;
+    for (int j = 0; j < 4; ++j) {
+      if ((tq >> j) & 1) {
+        if (rank < need_n) keep |= 1u << (4 * q + j);
+        ++rank;
+      }
     }
-    const uint64_t rank = base + before + __popcll(b & lanemask_lt());
-    if (((ties >> i) & 1) && rank < need_n) keep |= 1u << i;
-    base += tot;
+    base += total;
   }
-  __syncthreads();  // cnt may be reused
   return keep;
 }
 
-template <int EPL>
-__device__ int select_and_draw(const HeadView &hv, const StepView &sv, const float *sc,
-                               bool greedy, int top_k, float top_p, uint64_t rkey, int t, int k,
-                               Smem<EPL> &sm) {
-  static_assert(EPL <= 32, "one bit per element in a 32-bit mask");
-  const int tid = threadIdx.x;
-  const int V = hv.V;
-  float x[EPL];
-  uint32_t active = 0;
+// ---- selection through the bins ------------------------------------------------
+// The wave scans the histogram h[0..kBins) (8 bins per lane) and returns the
+// first bin whose cumulative count/mass reaches `target` (kBins: the open bin),
+// with the cumulative value of the bins before it and the bin's own value.
+template <typename T>
+__device__ __forceinline__ int find_cut_bin(const T *h, uint64_t target, uint64_t &above,
+                                            uint64_t &inbin, uint64_t total) {
+  const int lane = lane_id();
+  uint64_t v[8], lsum = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[j] = (uint64_t)h[8 * lane + j];
+    lsum += v[j];
+  }
+  const uint64_t incl = wave_incl_add_u64(lsum);
+  const uint64_t excl = incl - lsum;
+  const uint64_t bal = __ballot(excl < target && incl >= target);
+  if (bal == 0) {
+    above = readlane_u64(incl, 63);
+    inbin = total - above;
+    return kBins;
+  }
+  const int src = __ffsll((long long)bal) - 1;
+  uint64_t cum = readlane_u64(excl, src);
+  int b = 0;
+  above = cum;
+  inbin = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint64_t vj = readlane_u64(v[j], src);
+    if (inbin == 0 && cum + vj >= target) {
+      b = 8 * src + j;
+      above = cum;
+      inbin = vj;
+    }
+    cum += vj;
+  }
+  return b;
+}
+
+template <int GPT>
+__device__ __forceinline__ void bins_of(const float (&x)[4 * GPT], uint32_t active, float mx,
+                                        int (&bin)[4 * GPT]) {
+#pragma unroll
+  for (int i = 0; i < 4 * GPT; ++i) {
+    const float d = (mx - x[i]) * kBinScale;   // monotone in x
+    bin[i] = ((active >> i) & 1) ? (d < (float)kBins ? (int)d : kBins) : -1;
+  }
+}
+
+// Rank the listed elements of a cut bin by (score desc, id asc); n <= kCap.
+template <int GPT>
+__device__ __forceinline__ void rank_list(Smem<GPT> &sm, int n) {
+  const int t = threadIdx.x;
+  if (t < n) {
+    const float v = sm.lv[t];
+    const int id = sm.li[t];
+    int r = 0;
+    for (int j = 0; j < n; ++j) {
+      const float o = sm.lv[j];
+      r += (o > v || (o == v && sm.li[j] < id)) ? 1 : 0;
+    }
+    sm.lr[t] = r;
+  }
+}
+
+template <int GPT>
+__device__ __forceinline__ uint32_t radix_topk(const float (&x)[4 * GPT], uint32_t active, int top_k,
+                                            Smem<GPT> &sm, int &slot, int &pass) {
+  const Cut c = radix_select<GPT, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
+  return apply_cut<GPT>(x, active, c, c.need, sm, slot);
+}
+
+template <int GPT>
+__device__ __forceinline__ uint32_t radix_topp(const float (&x)[4 * GPT], uint32_t active,
+                                            const uint64_t (&mass)[4 * GPT], uint64_t target,
+                                            Smem<GPT> &sm, int &slot, int &pass) {
+  const Cut c = radix_select<GPT, true>(x, active, mass, target, sm, pass);
+  uint64_t need_n = 0;
+  if (c.exact) {
+    // every element tied at kappa carries the same mass q: the fewest reaching rem
+    uint64_t q = 0;
+#pragma unroll
+    for (int i = 0; i < 4 * GPT; ++i)
+      if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass[i];
+    // every nonzero q is the same value, so the halves reduce independently
+    const uint64_t qhi = block_max_u32((uint32_t)(q >> 32), sm, slot);
+    const uint64_t qlo = block_max_u32((uint32_t)q, sm, slot);
+    q = qhi << 32 | qlo;
+    need_n = q ? (c.need + q - 1) / q : 1;
+  }
+  return apply_cut<GPT>(x, active, c, need_n, sm, slot);
+}
+
+template <int GPT>
+__device__ __forceinline__ void zero_radix(Smem<GPT> &sm) {
+#pragma unroll
+  for (int b = 0; b < 2; ++b) sm.hist[b][threadIdx.x] = 0;
+  __syncthreads();
+}
+
+// top-k over the active set; `mx` is the maximum active score
+template <int GPT>
+__device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint32_t active,
+                                                float mx, int top_k, Smem<GPT> &sm, int &slot,
+                                                int &pass, int V) {
+  constexpr int EPL = 4 * GPT;
+  int bin[EPL];
+  bins_of<GPT>(x, active, mx, bin);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.cnt[bin[i]], 1u);
+  __syncthreads();
+  uint64_t above, inbin;
+  const int bc = find_cut_bin(sm.cnt, (uint64_t)top_k, above, inbin, (uint64_t)V);
+  const uint64_t need = (uint64_t)top_k - above;
+  uint32_t keep = 0;
+  if (bc < kBins && need == inbin) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (bin[i] >= 0 && bin[i] <= bc) keep |= 1u << i;
+    return keep;
+  }
+  if (bc == kBins || inbin > (uint64_t)kCap) {
+    zero_radix(sm);
+    return radix_topk<GPT>(x, active, top_k, sm, slot, pass);
+  }
+  int my[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    const int e = i * kThreads + tid;
-    x[i] = (e < V) ? sc[e] : -INFINITY;
-    if (e < V) active |= 1u << i;
+    my[i] = -1;
+    if (bin[i] == bc) {
+      const int s = (int)atomicAdd(&sm.lcount, 1u);
+      sm.lv[s] = x[i];
+      sm.li[s] = 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4);
+      my[i] = s;
+    }
   }
-  int slot = 0;
-  if (greedy) {
-    float bv = -INFINITY;
-    int bi = INT32_MAX;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if ((active >> i) & 1) keep_better(bv, bi, x[i], i * kThreads + tid);
-    return block_argmax(bv, bi, sm, slot);
-  }
-  // histograms 0 and 1 zero, kept mask zero
-#pragma unroll
-  for (int b = 0; b < 2; ++b) sm.hist[b][tid] = 0;
-  for (int w = tid; w < (EPL * kThreads + 31) / 32; w += kThreads) sm.kept[w] = 0;
   __syncthreads();
-  int pass = 0;
-  if (top_k > 0 && top_k < V) {
-    const Cut c = radix_select<EPL, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
-    active = apply_cut<EPL>(x, active, c, c.need, sm, slot);
+  rank_list(sm, (int)inbin);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    if (bin[i] >= 0 && (bin[i] < bc || (my[i] >= 0 && (uint64_t)sm.lr[my[i]] < need)))
+      keep |= 1u << i;
+  if (threadIdx.x == 0) sm.lcount = 0;   // next read follows at least one barrier
+  return keep;
+}
+
+// top-p over the active set (the survivors of top-k); `mx` is their maximum
+template <int GPT>
+__device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint32_t active,
+                                                float mx, float top_p, Smem<GPT> &sm, int &slot,
+                                                int &pass) {
+  constexpr int EPL = 4 * GPT;
+  // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
+  // converted exactly to a 64-bit integer
+  uint64_t mass[EPL];
+  uint64_t zl = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
+    zl += mass[i];
   }
-  if (top_p < 1.0f) {
-    float mloc = -INFINITY;
+  const uint64_t Z = block_sum_u64(zl, sm, slot);
+  uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
+  if (target < 1) target = 1;
+  if (target > Z) return active;
+  int bin[EPL];
+  bins_of<GPT>(x, active, mx, bin);
 #pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if ((active >> i) & 1) mloc = fmaxf(mloc, x[i]);
-    // the max through the order key (monotone), reduced as an integer
-    const uint32_t mk = (uint32_t)block_max_u64((uint64_t)order_key(mloc), sm, slot);
-    slot ^= 1;
-    const uint32_t mu = (mk & 0x80000000u) ? (mk & 0x7FFFFFFFu) : ~mk;
-    const float mx = __uint_as_float(mu);
-    // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
-    // converted exactly to a 64-bit integer
-    uint64_t mass[EPL];
-    uint64_t zl = 0;
+  for (int i = 0; i < EPL; ++i)
+    if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.mh[bin[i]], (unsigned long long)mass[i]);
+  __syncthreads();
+  uint64_t above, inbin;
+  const int bc = find_cut_bin(sm.mh, target, above, inbin, Z);
+  if (bc == kBins) {
+    zero_radix(sm);
+    return radix_topp<GPT>(x, active, mass, target, sm, slot, pass);
+  }
+  int my[EPL];
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
-      zl += mass[i];
-    }
-    const uint64_t Z = block_sum_u64(zl, sm, slot);
-    slot ^= 1;
-    uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
-    if (target < 1) target = 1;
-    if (target <= Z) {
-      const Cut c = radix_select<EPL, true>(x, active, mass, target, sm, pass);
-      uint64_t need_n = 0;
-      if (c.exact) {
-        // every element tied at kappa carries the same mass q: the fewest reaching rem
-        uint64_t q = 0;
-#pragma unroll
-        for (int i = 0; i < EPL; ++i)
-          if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass[i];
-        q = block_max_u64(q, sm, slot);
-        slot ^= 1;
-        need_n = q ? (c.need + q - 1) / q : 1;
+  for (int i = 0; i < EPL; ++i) {
+    my[i] = -1;
+    if (bin[i] == bc) {
+      const int s = (int)atomicAdd(&sm.lcount, 1u);
+      if (s < kCap) {
+        sm.lv[s] = x[i];
+        sm.li[s] = 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4);
+        sm.lm[s] = mass[i];
+        my[i] = s;
       }
-      active = apply_cut<EPL>(x, active, c, need_n, sm, slot);
     }
   }
-  // kept-id bitmask, then one Philox block per group of 4 consecutive ids
+  __syncthreads();
+  const int n = (int)sm.lcount;
+  if (n > kCap) {
+    __syncthreads();   // everyone has read lcount
+    if (threadIdx.x == 0) sm.lcount = 0;
+    zero_radix(sm);
+    return radix_topp<GPT>(x, active, mass, target, sm, slot, pass);
+  }
+  rank_list(sm, n);
+  __syncthreads();
+  if ((int)threadIdx.x < n) sm.lsm[sm.lr[threadIdx.x]] = sm.lm[threadIdx.x];
+  __syncthreads();
+  // entry kept iff the mass strictly before it (in rank order) is below target
+  if ((int)threadIdx.x < n) {
+    uint64_t before = above;
+    for (int r = 0; r < sm.lr[threadIdx.x]; ++r) before += sm.lsm[r];
+    sm.lr[threadIdx.x] = before < target ? 1 : 0;
+  }
+  __syncthreads();
+  uint32_t keep = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    if (bin[i] >= 0 && (bin[i] < bc || (my[i] >= 0 && sm.lr[my[i]] != 0))) keep |= 1u << i;
+  if (threadIdx.x == 0) sm.lcount = 0;
+  return keep;
+}
+
+template <int GPT>
+__device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
+                                               uint32_t active, int V, bool greedy, int top_k,
+                                               float top_p, uint64_t rkey, int t, int k,
+                                               Smem<GPT> &sm, int &slot) {
+  constexpr int EPL = 4 * GPT;
+  const int tid = threadIdx.x;
+  uint32_t mk = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
     if ((active >> i) & 1) {
-      const int e = i * kThreads + tid;
-      atomicOr(&sm.kept[e >> 5], 1u << (e & 31));
+      const uint32_t key = order_key(x[i]);
+      mk = key > mk ? key : mk;
     }
-  __syncthreads();
+  mk = block_max_u32(mk, sm, slot);   // also publishes the zeroed histograms
+  if (greedy) {
+    uint32_t id = 0xFFFFFFFFu;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (((active >> i) & 1) && order_key(x[i]) == mk) {
+        const uint32_t e = 4u * (uint32_t)((i / 4) * kThreads + tid) + (uint32_t)(i % 4);
+        id = e < id ? e : id;
+      }
+    return (int)block_min_u32(id, sm, slot);
+  }
+  const float mx = key_to_float(mk);
+  int pass = 0;
+  uint32_t kept = active;
+  if (top_k > 0 && top_k < V) kept = select_topk<GPT>(x, kept, mx, top_k, sm, slot, pass, V);
+  if (top_p < 1.0f) kept = select_topp<GPT>(x, kept, mx, top_p, sm, slot, pass);
+  // Gumbel-max over the kept ids, one Philox block per group with a kept id
   double bv = -INFINITY;
   int bi = INT32_MAX;
-  const int groups = (V + 3) >> 2;
-  for (int g = tid; g < groups; g += kThreads) {
-    const uint32_t bits = (sm.kept[g >> 3] >> ((g & 7) * 4)) & 0xFu;
-    if (!bits) continue;
-    const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if ((bits >> j) & 1) {
-        const int v = 4 * g + j;
-        const double val = (double)sc[v] + (double)gumbel_from_word(w.w[j]);
-        keep_better(bv, bi, val, v);
-      }
+  for (int q = 0; q < GPT; ++q) {
+    const uint32_t bits = (kept >> (4 * q)) & 0xFu;
+    if (bits) {
+      const int g = q * kThreads + tid;
+      const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if ((bits >> j) & 1)
+          keep_better(bv, bi, (double)x[4 * q + j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
+    }
   }
-  return block_argmax(bv, bi, sm, slot);
+  return block_argmax_f64(bv, bi, sm, slot);
 }
 
-template <int EPL>
+template <int GPT>
 __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView sv,
                                                           int with_text) {
-  __shared__ Smem<EPL> sm;
+  constexpr int EPL = 4 * GPT;
+  __shared__ Smem<GPT> sm;
   const int tid = threadIdx.x;
   const int vec = blockIdx.x;
+  const int n_audio = sv.Rs * hv.K;
+  // histograms start at zero (published by the first block reduction)
+  for (int b = tid; b <= kBins; b += kThreads) {
+    sm.cnt[b] = 0;
+    sm.mh[b] = 0;
+  }
+  if (tid == 0) sm.lcount = 0;
+  int slot = 0;
+
+  // The scores depend only on the vector index: load them before anything
+  // else so that their latency overlaps the plan and parameter loads.
+  float x[EPL];
+  uint32_t active = 0;
+  const int V = hv.V;
+  if (vec < n_audio) {
+    const int s = vec / hv.K, k = vec % hv.K;
+    const float *sc = sv.scores + (size_t)s * hv.N + (size_t)k * V;
+    if ((V & 3) == 0) {
+#pragma unroll
+      for (int q = 0; q < GPT; ++q) {
+        const int g = q * kThreads + tid;
+        float4 v = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        if (4 * g < V) v = *reinterpret_cast<const float4 *>(sc + 4 * g);
+        x[4 * q + 0] = v.x;
+        x[4 * q + 1] = v.y;
+        x[4 * q + 2] = v.z;
+        x[4 * q + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        const int e = 4 * ((i / 4) * kThreads + tid) + (i % 4);
+        x[i] = e < V ? sc[e] : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = 4 * ((i / 4) * kThreads + tid) + (i % 4);
+      if (e < V) active |= 1u << i;
+    }
+  }
+
   if (!plan_ok(sv)) {
     if (vec == 0 && tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
     return;
   }
   const int32_t *rows = sv.plan + kPlanHeader;
-  const int n_audio = sv.Rs * hv.K;
   if (vec >= n_audio) {
     // text row: reduce the (max, lowest argmax) partials of the text GEMM
     const int j = vec - n_audio;
@@ -405,7 +743,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     for (int p = tid; p < sv.text_parts; p += kThreads)
       keep_better(bv, bi, sv.text_val[(size_t)j * sv.text_parts + p],
                   sv.text_idx[(size_t)j * sv.text_parts + p]);
-    const int tok = block_argmax(bv, bi, sm, 0);
+    const int tok = block_argmax_f32(bv, bi, sm, slot);
     for (int k = tid; k < hv.K; k += kThreads)
       sv.tokens_out[(size_t)r * hv.K + k] = (k == 0) ? tok : hv.pad_id;
     return;
@@ -431,29 +769,29 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     if (bad) {
       if (tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
-      const float *sc = sv.scores + (size_t)s * hv.N + (size_t)k * hv.V;
       const uint64_t rkey = sv.rng_key ? sv.rng_key[r] : (uint64_t)r;
-      token = select_and_draw<EPL>(hv, sv, sc, T == 0.0f, sv.top_k[r], P, rkey, t, k, sm);
+      token = select_and_draw<GPT>(sv, x, active, V, T == 0.0f, sv.top_k[r], P, rkey, t, k, sm,
+                                   slot);
       sampled = true;
     }
   }
   if (tid == 0) {
     sv.tokens_out[(size_t)r * hv.K + k] = token;
     if (u >= 0) sv.tokens_out[(size_t)u * hv.K + k] = token;
-    const int slot = sv.grid_slot[r];
-    if (sampled && slot >= 0 && sv.frame_grid) {
-      if (slot < sv.n_slots && f < sv.F_max)
-        sv.frame_grid[((size_t)slot * hv.K + k) * sv.F_max + f] = token;
+    const int gslot = sv.grid_slot[r];
+    if (sampled && gslot >= 0 && sv.frame_grid) {
+      if (gslot < sv.n_slots && f < sv.F_max)
+        sv.frame_grid[((size_t)gslot * hv.K + k) * sv.F_max + f] = token;
       else
         atomicOr(sv.status, (uint32_t)MCD_DEV_GRID_RANGE);
     }
   }
 }
 
-template <int EPL>
-hipError_t launch_epl(const HeadView &hv, const StepView &sv, int nblk, bool with_text,
+template <int GPT>
+hipError_t launch_gpt(const HeadView &hv, const StepView &sv, int nblk, bool with_text,
                       hipStream_t st) {
-  hipLaunchKernelGGL(sample_kernel<EPL>, dim3(nblk), dim3(kThreads), 0, st, hv, sv,
+  hipLaunchKernelGGL(sample_kernel<GPT>, dim3(nblk), dim3(kThreads), 0, st, hv, sv,
                      (int)with_text);
   return hipGetLastError();
 }
@@ -464,12 +802,10 @@ hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t st) {
   const int nblk = sv.Rs * hv.K + (with_text ? sv.n_text : 0);
   if (nblk == 0) return hipSuccess;
-  const int epl = (hv.V + kThreads - 1) / kThreads;
-  if (epl <= 1) return launch_epl<1>(hv, sv, nblk, with_text, st);
-  if (epl <= 2) return launch_epl<2>(hv, sv, nblk, with_text, st);
-  if (epl <= 4) return launch_epl<4>(hv, sv, nblk, with_text, st);
-  if (epl <= 8) return launch_epl<8>(hv, sv, nblk, with_text, st);
-  if (epl <= 16) return launch_epl<16>(hv, sv, nblk, with_text, st);
+  const int groups = (hv.V + 3) / 4;
+  if (groups <= kThreads) return launch_gpt<1>(hv, sv, nblk, with_text, st);
+  if (groups <= 2 * kThreads) return launch_gpt<2>(hv, sv, nblk, with_text, st);
+  if (groups <= 4 * kThreads) return launch_gpt<4>(hv, sv, nblk, with_text, st);
   return hipErrorInvalidValue;
 }
 

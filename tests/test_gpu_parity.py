@@ -103,6 +103,13 @@ RAGGED = [
                          dtype="bf16", top_p=0.9, cfg_w=2.0, steps=4, shuffle=True)),
     ("stream_bm128", dict(H=768, K=4, V=129, n_pairs=55, n_solo=3, n_text=100, V_text=515,
                           dtype="bf16", top_k=20, steps=5)),
+    # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
+    ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
+                                temperature=0.9, steps=4, shuffle=True)),
+    ("mfma_xcd_remap", dict(H=192, K=4, V=128, n_pairs=200, n_solo=112, dtype="bf16", top_p=0.9,
+                            cfg_w=2.5, steps=4)),
+    ("mfma_text_rows", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=300,
+                            dtype="bf16", top_k=5, steps=3, shuffle=True)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
                               dtype="f32", top_k=5, top_p=0.8, steps=5, shuffle=True)),
     ("bf16_greedy", dict(H=64, K=4, V=100, n_pairs=5, n_solo=4, dtype="bf16", temperature=0.0,
