@@ -162,20 +162,33 @@ struct Smem {
   uint32_t cnt[kBins + 1];               // top-k bin counts
   unsigned long long mh[kBins + 1];      // top-p bin masses
   // elements of the cut bin, and their exact ranks
-  float lv[kCap];
-  int li[kCap];
-  unsigned long long lm[kCap];
+  struct Entry {
+    float v;
+    int id;
+  };
+  Entry le[kCap];
+  unsigned long long lm[kCap];           // their masses (top-p)
   int lr[kCap];
-  unsigned long long lsm[kCap];          // masses in rank order
+  unsigned long long lsm[kCap];          // masses in rank order, then the mass before each rank
+  uint32_t keepbits[kThreads];           // kept cut-bin elements, one bit per slot of a thread
   uint32_t lcount;
   // block reductions (two slots, alternating, one barrier each)
   uint32_t ru[2][kWaves];
   unsigned long long r64[2][kWaves];
   double rd[2][kWaves];
   int ri[2][kWaves];
-  // radix select (fallback)
+  // radix select (fallback); reused for the draw list once the selection is done
   unsigned long long hist[3][256];
 };
+
+// A group of four ids with kept members, moved to the thread that draws it.
+struct DrawItem {
+  int g;
+  uint32_t bits;
+  float x[4];
+};
+constexpr int kDrawCap = 256;
+static_assert(kDrawCap * sizeof(DrawItem) <= 3 * 256 * sizeof(unsigned long long), "draw list fits");
 
 template <int GPT>
 __device__ __forceinline__ uint32_t block_max_u32(uint32_t x, Smem<GPT> &sm, int &slot) {
@@ -230,6 +243,20 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t &to
   slot ^= 1;
   total = tot;
   return before + incl - x;
+}
+
+// inclusive prefix of x over the threads in id order
+template <int GPT>
+__device__ __forceinline__ uint64_t block_incl_scan_u64(uint64_t x, Smem<GPT> &sm, int &slot) {
+  const uint64_t incl = wave_incl_add_u64(x);
+  if (lane_id() == 63) sm.r64[slot][wave_id()] = incl;
+  __syncthreads();
+  uint64_t before = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w)
+    if (w < wave_id()) before += sm.r64[slot][w];
+  slot ^= 1;
+  return before + incl;
 }
 
 template <int GPT>
@@ -459,17 +486,28 @@ __device__ __forceinline__ void bins_of(const float (&x)[4 * GPT], uint32_t acti
 // Rank the listed elements of a cut bin by (score desc, id asc); n <= kCap.
 template <int GPT>
 __device__ __forceinline__ void rank_list(Smem<GPT> &sm, int n) {
+  using Entry = typename Smem<GPT>::Entry;
   const int t = threadIdx.x;
   if (t < n) {
-    const float v = sm.lv[t];
-    const int id = sm.li[t];
-    int r = 0;
-    for (int j = 0; j < n; ++j) {
-      const float o = sm.lv[j];
-      r += (o > v || (o == v && sm.li[j] < id)) ? 1 : 0;
+    const Entry me = sm.le[t];
+    auto ahead = [&](const Entry &o) __attribute__((always_inline)) {
+      return (int)((o.v > me.v) | ((o.v == me.v) & (o.id < me.id)));
+    };
+    int r = 0, j = 0;
+    for (; j + 4 <= n; j += 4) {
+      const Entry o0 = sm.le[j], o1 = sm.le[j + 1], o2 = sm.le[j + 2], o3 = sm.le[j + 3];
+      r += ahead(o0) + ahead(o1) + ahead(o2) + ahead(o3);
     }
+    for (; j < n; ++j) r += ahead(sm.le[j]);
     sm.lr[t] = r;
   }
+}
+
+// Thread that owns id e, and the slot of e in its registers.
+__device__ __forceinline__ void owner_of(int e, int &thread, int &slot) {
+  const int g = e >> 2;
+  thread = g % kThreads;
+  slot = 4 * (g / kThreads) + (e & 3);
 }
 
 template <int GPT>
@@ -533,25 +571,27 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
     zero_radix(sm);
     return radix_topk<GPT>(x, active, top_k, sm, slot, pass);
   }
-  int my[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    my[i] = -1;
     if (bin[i] == bc) {
       const int s = (int)atomicAdd(&sm.lcount, 1u);
-      sm.lv[s] = x[i];
-      sm.li[s] = 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4);
-      my[i] = s;
+      sm.le[s] = {x[i], 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4)};
     }
   }
   __syncthreads();
   rank_list(sm, (int)inbin);
+  if ((int)threadIdx.x < (int)inbin && (uint64_t)sm.lr[threadIdx.x] < need) {
+    int ow, sl;
+    owner_of(sm.le[threadIdx.x].id, ow, sl);
+    atomicOr(&sm.keepbits[ow], 1u << sl);
+  }
   __syncthreads();
+  keep = sm.keepbits[threadIdx.x];
+  sm.keepbits[threadIdx.x] = 0;          // next use follows at least one barrier
+  if (threadIdx.x == 0) sm.lcount = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if (bin[i] >= 0 && (bin[i] < bc || (my[i] >= 0 && (uint64_t)sm.lr[my[i]] < need)))
-      keep |= 1u << i;
-  if (threadIdx.x == 0) sm.lcount = 0;   // next read follows at least one barrier
+    if (bin[i] >= 0 && bin[i] < bc) keep |= 1u << i;
   return keep;
 }
 
@@ -586,17 +626,13 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
     zero_radix(sm);
     return radix_topp<GPT>(x, active, mass, target, sm, slot, pass);
   }
-  int my[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    my[i] = -1;
     if (bin[i] == bc) {
       const int s = (int)atomicAdd(&sm.lcount, 1u);
       if (s < kCap) {
-        sm.lv[s] = x[i];
-        sm.li[s] = 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4);
+        sm.le[s] = {x[i], 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4)};
         sm.lm[s] = mass[i];
-        my[i] = s;
       }
     }
   }
@@ -612,18 +648,24 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
   __syncthreads();
   if ((int)threadIdx.x < n) sm.lsm[sm.lr[threadIdx.x]] = sm.lm[threadIdx.x];
   __syncthreads();
+  // mass of the ranks before each rank: a block scan (thread r holds rank r)
+  const uint64_t mr = (int)threadIdx.x < n ? sm.lsm[threadIdx.x] : 0;
+  const uint64_t incl = block_incl_scan_u64(mr, sm, slot);
+  if ((int)threadIdx.x < n) sm.lsm[threadIdx.x] = incl - mr;   // every read of lsm is done
+  __syncthreads();
   // entry kept iff the mass strictly before it (in rank order) is below target
-  if ((int)threadIdx.x < n) {
-    uint64_t before = above;
-    for (int r = 0; r < sm.lr[threadIdx.x]; ++r) before += sm.lsm[r];
-    sm.lr[threadIdx.x] = before < target ? 1 : 0;
+  if ((int)threadIdx.x < n && above + sm.lsm[sm.lr[threadIdx.x]] < target) {
+    int ow, sl;
+    owner_of(sm.le[threadIdx.x].id, ow, sl);
+    atomicOr(&sm.keepbits[ow], 1u << sl);
   }
   __syncthreads();
-  uint32_t keep = 0;
+  uint32_t keep = sm.keepbits[threadIdx.x];
+  sm.keepbits[threadIdx.x] = 0;
+  if (threadIdx.x == 0) sm.lcount = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if (bin[i] >= 0 && (bin[i] < bc || (my[i] >= 0 && sm.lr[my[i]] != 0))) keep |= 1u << i;
-  if (threadIdx.x == 0) sm.lcount = 0;
+    if (bin[i] >= 0 && bin[i] < bc) keep |= 1u << i;
   return keep;
 }
 
@@ -660,6 +702,31 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
   // Gumbel-max over the kept ids, one Philox block per group with a kept id
   double bv = -INFINITY;
   int bi = INT32_MAX;
+  if (top_k > 0 && top_k <= kDrawCap) {
+    // few kept groups: move them to one thread each, so that no wave runs
+    // several Philox blocks one after another
+    uint32_t n = 0;
+#pragma unroll
+    for (int q = 0; q < GPT; ++q) n += ((kept >> (4 * q)) & 0xFu) ? 1u : 0u;
+    uint32_t total;
+    uint32_t pos = block_excl_scan_u32(n, total, sm, slot);
+    DrawItem *dl = reinterpret_cast<DrawItem *>(&sm.hist[0][0]);
+#pragma unroll
+    for (int q = 0; q < GPT; ++q) {
+      const uint32_t bits = (kept >> (4 * q)) & 0xFu;
+      if (bits) dl[pos++] = {q * kThreads + tid, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
+    }
+    __syncthreads();
+    if (tid < (int)total) {
+      const DrawItem it = dl[tid];
+      const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)it.g);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if ((it.bits >> j) & 1)
+          keep_better(bv, bi, (double)it.x[j] + (double)gumbel_from_word(w.w[j]), 4 * it.g + j);
+    }
+    return block_argmax_f64(bv, bi, sm, slot);
+  }
 #pragma unroll
   for (int q = 0; q < GPT; ++q) {
     const uint32_t bits = (kept >> (4 * q)) & 0xFu;
@@ -688,6 +755,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     sm.cnt[b] = 0;
     sm.mh[b] = 0;
   }
+  sm.keepbits[tid] = 0;
   if (tid == 0) sm.lcount = 0;
   int slot = 0;
 
