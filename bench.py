@@ -39,11 +39,17 @@ COPY_PROBE_BYTES = 2**30       # --copy-probe: one plain device copy of this man
 # HBM traffic of the head projection kernel per launch, from two rocprofv3 --pmc
 # passes (FETCH_SIZE, then WRITE_SIZE) over `bench.py --copy-probe`, each
 # counter scaled by what it reads for the probe's plain copy of known size.
-# Valid only for the kernel source it was taken on (sha256 below); a changed
-# kernel reports traffic null until the counters are taken again.
-K1_SOURCE = os.path.join(ROOT, "paper_2607_02119_amd", "csrc", "k_head_gemm.hip")
+# Valid only for the kernel sources it was taken on (sha256 over the listed
+# files); a changed kernel reports traffic null until the counters are taken
+# again.
+CSRC = os.path.join(ROOT, "paper_2607_02119_amd", "csrc")
 MEASURED_TRAFFIC = {
-    # workload: dict(k1_sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
+    # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
+    "weight_streaming": dict(
+        sources=["k_stream.hip", "gemm_common.h"],
+        sha256="e77f374eb66fb715f2b719a8bbd222fe46cba68ca158988f02f44f0253f1ea34",
+        fetch_bytes=278410679, write_bytes=8388608,
+        profile="profiles/head_step_weight_streaming.md"),
 }
 
 
@@ -58,16 +64,21 @@ def algorithmic(wl):
                 scores_bytes=4 * wl.Rs * wl.N)
 
 
+def sources_sha256(names):
+    import hashlib
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(CSRC, n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def k1_traffic(workload):
     """Measured HBM bytes per head-projection launch, or None if not measured
-    for this workload or the kernel source changed since."""
-    import hashlib
+    for this workload or the kernel sources changed since."""
     m = MEASURED_TRAFFIC.get(workload)
-    if not m:
+    if not m or sources_sha256(m["sources"]) != m["sha256"]:
         return None
-    with open(K1_SOURCE, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != m["k1_sha256"]:
-            return None
     return m["fetch_bytes"] + m["write_bytes"]
 
 

@@ -18,7 +18,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmcd.so")
 ARCH = "gfx950"
 
-SOURCES = ["mcd_api.cpp", "k_head_gemm.hip", "k_sample.hip", "k_grid.hip"]
+SOURCES = ["mcd_api.cpp", "k_head_gemm.hip", "k_stream.hip", "k_mfma.hip", "k_sample.hip",
+           "k_grid.hip"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra",

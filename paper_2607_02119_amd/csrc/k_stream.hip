@@ -1,0 +1,260 @@
+// K1, weight-streaming path (at most 128 GEMM rows): codebook-head projection
+// with the CFG merge and temperature fused into the epilogue, or the text-head
+// projection with a fused (max, lowest argmax) epilogue.
+//
+//   logits[g][n] = sum_h hidden[row(g)][h] * W[n][h]         (Sec. 2.1, n = k*V + v)
+//   pair p (GEMM rows 2p, 2p+1 = Main, Companion):
+//     scores[p][n] = (w * l_main + (1 - w) * l_comp) / T    (Eq. 1, Sec. 2.4)
+//   solo row j:  scores[n_pairs + j][n] = l / T;  T = 0 (greedy): no division
+//   text rows:   per row and 32-column part, the largest logit and its lowest id.
+#include "gemm_common.h"
+
+namespace mcd {
+namespace {
+
+// Weight-streaming path for up to 128 rows, staged with direct global->LDS
+// loads.  A workgroup owns all BM rows and BN columns.  Each k slice of SK = 64
+// (128 bytes of every weight and hidden row) is copied into one of S LDS
+// stages by global_load_lds_dwordx4 (64 lanes x 16 B, eight 128-byte row
+// segments per instruction), S - 1 slices ahead of its use, without passing
+// through registers.  Waves split the tile 2 x 2: column half (w & 1) and the
+// k32 half (w >> 1) of every slice; the two k halves meet in LDS at the end.
+//
+// LDS layout of a slice: [rows][8 chunks of 16 B]; chunk c of row r is stored
+// at position c ^ ((r >> 1) & 7), so the 16 rows of an MFMA fragment read hit
+// 16 distinct bank groups.  The loop waits for the copies explicitly (vector
+// memory counter: only these copies are outstanding in the loop); slices past
+// the end re-load the last slice (clamped) so that every iteration issues the
+// same count, and a copy only ever targets the stage read S - 1 iterations
+// earlier, after a barrier that follows every wave's reads of it.
+constexpr int kDmaSK = 64;                 // k per slice
+constexpr int kDmaLdsBudget = 144 * 1024;  // bytes of LDS for the two rings
+
+template <int BM, int BN, bool TEXT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void head_gemm_dma(
+    HeadView hv, StepView sv) {
+  constexpr int SK = kDmaSK;
+  constexpr int MB = BM / 32;              // 32-row MFMA blocks: all rows of the tile
+  constexpr int WN = BN / 2;               // columns per wave
+  constexpr int NB = WN / 32;              // 32-column MFMA blocks per wave
+  constexpr int ROWB = SK * 2;             // bytes of one row segment (128)
+  constexpr int WST = BN * ROWB, AST = BM * ROWB;
+  // Waves 0-1 copy weight slices, waves 2-3 hidden-state slices.  Vector
+  // memory operations of one wave complete in issue order, so a wave that
+  // issued only weight copies can keep SW - 1 of them in flight without
+  // waiting behind the (faster, L2-resident) hidden-state copies.
+  constexpr int SA = 3;                                           // hidden-state stages
+  constexpr int SW0 = (kDmaLdsBudget - SA * AST) / WST;
+  constexpr int SW = SW0 > 8 ? 8 : SW0;                           // weight stages
+  constexpr int WIW = WST / 1024 / 2;      // copy instructions per weight wave per slice
+  constexpr int AIA = AST / 1024 / 2;      // per hidden-state wave per slice
+  static_assert(SW >= 3 && WIW >= 1 && AIA >= 1 && MB >= 1 && NB >= 1, "tile shape");
+  static_assert((SW - 2) * WIW < 64 && (SA - 2) * AIA < 64, "vmcnt range");
+
+  __shared__ __attribute__((aligned(1024))) char lds[SW * WST + SA * AST];
+  char *const wring = lds;                 // weight stages
+  char *const aring = lds + SW * WST;      // hidden-state stages
+  // per pair of GEMM rows (2q, 2q + 1): {w, 1/T, out, -2} for a CFG pair,
+  // {1/T_0, 1/T_1, out_0, out_1} for two solo rows (out -1: no row)
+  __shared__ float4 rowp[BM / 2];
+
+  const int32_t *rows = sv.plan + kPlanHeader + (TEXT ? sv.Mg : 0);
+  const int M = TEXT ? sv.n_text : sv.Mg;
+  const int N = TEXT ? hv.V_text : hv.N;
+  const __bf16 *Wp = static_cast<const __bf16 *>(TEXT ? hv.W_text : hv.W);
+  const __bf16 *X = static_cast<const __bf16 *>(sv.hidden);
+  const int H = hv.H;
+  const int NST = H / SK;
+
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tile_m = blockIdx.x % tiles_m;
+  const int tile_n = blockIdx.x / tiles_m;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ch = wave & 1, kh = wave >> 1;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const bool w_copier = wave_s < 2;        // wave-uniform role
+
+  // Each tile walks the k slices starting at its own offset, so that at any
+  // moment the workgroups read different offsets of their (8 KiB-strided)
+  // weight rows and spread over the HBM channels instead of all hitting the
+  // same ones.  The sum order per tile is fixed, so results stay deterministic.
+  const int kskew = (int)(((unsigned)tile_n * 7u) % (unsigned)NST);
+  const uint32_t wbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)wring;
+  const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)aring;
+  const int seg_r = lane >> 3, seg_c = lane & 7;
+
+  // Per-lane global sources of this wave's copy instructions (chunk-swizzled):
+  // a weight wave copies rows (wave * WIW + q) * 8 .. +7 of the tile, a
+  // hidden-state wave rows ((wave - 2) * AIA + q) * 8 .. +7.
+  constexpr int QN = WIW > AIA ? WIW : AIA;
+  const __bf16 *src[QN];
+  // copy slice st (clamped to the last one) into its stage
+  auto issue_w = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = wbase + (uint32_t)((st % SW) * WST);
+    static_for<0, WIW>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16_stream(src[q] + ks * SK, sb + (uint32_t)((wave_s * WIW + q) * 1024));
+    });
+  };
+  auto issue_a = [&](int st) __attribute__((always_inline)) {
+    int ks = min(st, NST - 1) + kskew;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t sb = abase + (uint32_t)((st % SA) * AST);
+    static_for<0, AIA>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+    });
+  };
+
+  // The weight waves start streaming at once: their copies depend on nothing
+  // but the tile, and nothing else is outstanding in their counters until the
+  // end of the loop.
+  wait_vmem_and_lds<0>();
+  if (w_copier) {
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < WIW) {
+        const int r = (wave_s * WIW + q) * 8 + seg_r;
+        const int n = min(n0 + r, N - 1);
+        src[q] = Wp + (size_t)n * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+      }
+    });
+#pragma unroll
+    for (int st = 0; st < SW - 1; ++st) issue_w(st);
+  }
+
+  if (!plan_ok(sv)) {
+    wait_vmem_and_lds<0>();  // no copy may still be landing in this workgroup's LDS
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    return;
+  }
+
+  if (!w_copier) {
+    // The hidden-state waves gather their rows through the plan, stage the
+    // per-row epilogue parameters in LDS, and wait for all of it before their
+    // first copy, so that only copies are outstanding in their loop counters.
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      src[q] = nullptr;
+      if (q < AIA) {
+        const int r = ((wave_s - 2) * AIA + q) * 8 + seg_r;
+        int pr = rows[min(m0 + r, M - 1)];
+        if (pr < 0 || pr >= sv.R) {
+          atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+          pr = 0;
+        }
+        src[q] = X + (size_t)pr * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+      }
+    });
+    const int q2 = tid - 128;
+    if (!TEXT && q2 < BM / 2) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
+    wait_vmem_and_lds<0>();
+#pragma unroll
+    for (int st = 0; st < SA - 1; ++st) issue_a(st);
+  }
+
+  floatx16 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Fragment byte offsets within a stage.  v_mfma_f32_32x32x16_bf16: lane l
+  // holds row (or column) l % 32 and the 8 consecutive k of chunk l / 32 of the
+  // k16 step; this wave covers k32 half kh of the slice (chunks 4kh .. 4kh+3).
+  const int frow = lane & 31;
+  int aoff[2][MB], woff[2][NB];
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const int c = 4 * kh + 2 * s2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const int r = i * 32 + frow;
+      aoff[s2][i] = r * ROWB + ((c ^ ((r >> 1) & 7)) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int r = ch * WN + j * 32 + frow;
+      woff[s2][j] = r * ROWB + ((c ^ ((r >> 1) & 7)) * 16);
+    }
+  }
+
+  for (int st = 0; st < NST; ++st) {
+    // this wave's copies of slice st have landed and its reads of slice st - 1
+    // are done; the barrier extends both to the whole workgroup
+    if (w_copier) wait_vmem_and_lds<(SW - 2) * WIW>();
+    else wait_vmem_and_lds<(SA - 2) * AIA>();
+    block_barrier_no_vmem_wait();
+    if (w_copier) issue_w(st + SW - 1);
+    else issue_a(st + SA - 1);
+    const char *wsb = wring + (st % SW) * WST;
+    const char *asb = aring + (st % SA) * AST;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      bf16x8 a[MB], b[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(asb + aoff[s2][i]);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = *reinterpret_cast<const bf16x8 *>(wsb + woff[s2][j]);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // the copies are invisible to the compiler: drain them before reusing LDS
+  wait_vmem_and_lds<0>();
+  __syncthreads();
+
+  // Epilogue, in two phases through LDS (the rings are free now).
+  // Phase 1: every wave writes its partial sums (its k half) to C[kh][row][col].
+  // Phase 2: each thread takes 16-byte column chunks (audio) or 32-column text
+  // parts of whole rows, adds the two k halves (a two-term sum: order-free),
+  // and applies the fused epilogue with coalesced stores.  No global load is
+  // left pending among the stores, so they never wait for each other.
+  constexpr int CP = BN + 4;               // padded row pitch of C (floats)
+  static_assert(2 * BM * CP * 4 <= SW * WST + SA * AST, "C fits the rings");
+  float *C = reinterpret_cast<float *>(lds);
+  static_for<0, MB * NB * 16>([&](auto fc) __attribute__((always_inline)) {
+    constexpr int f = decltype(fc)::value;
+    constexpr int i = f / (NB * 16), j = (f / 16) % NB, r = f % 16;
+    const int row = i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    C[(kh * BM + row) * CP + ch * WN + j * 32 + frow] = acc[i][j][r];
+  });
+
+  epilogue_from_lds<BM, BN, CP, TEXT, 2>(hv, sv, C, rowp, m0, n0, M, N);
+}
+
+template <int BM, int BN, bool TEXT>
+hipError_t launch_dma(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+  hipLaunchKernelGGL((head_gemm_dma<BM, BN, TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
+  return hipGetLastError();
+}
+
+// Weight-streaming launch for M <= 128 rows: 128-column tiles, or 64 when that
+// leaves fewer workgroups than compute units.
+template <bool TEXT>
+hipError_t launch_skinny(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  const bool narrow = (N + 127) / 128 < 256;
+  if (M <= 32) return narrow ? launch_dma<32, 64, TEXT>(hv, sv, M, N, st) : launch_dma<32, 128, TEXT>(hv, sv, M, N, st);
+  if (M <= 64) return narrow ? launch_dma<64, 64, TEXT>(hv, sv, M, N, st) : launch_dma<64, 128, TEXT>(hv, sv, M, N, st);
+  return narrow ? launch_dma<128, 64, TEXT>(hv, sv, M, N, st) : launch_dma<128, 128, TEXT>(hv, sv, M, N, st);
+}
+
+}  // namespace
+
+hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
+                              hipStream_t st) {
+  return text ? launch_skinny<true>(hv, sv, sv.n_text, hv.V_text, st)
+              : launch_skinny<false>(hv, sv, sv.Mg, hv.N, st);
+}
+
+}  // namespace mcd

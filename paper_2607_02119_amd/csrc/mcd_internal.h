@@ -64,6 +64,11 @@ inline int32_t text_parts_for(int32_t V_text) {
 
 // Kernel launchers (one .hip file each).
 hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t stream);
+// bf16 projection kernels (audio rows, or the text rows when text is set)
+hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
+                              hipStream_t stream);   // at most 128 GEMM rows
+hipError_t launch_mfma_gemm(const HeadView &hv, const StepView &sv, bool text,
+                            hipStream_t stream);     // any number of rows
 hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t stream);
 hipError_t launch_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,
