@@ -106,8 +106,12 @@ RAGGED = [
     # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
     ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
                                 temperature=0.9, steps=4, shuffle=True)),
-    ("mfma_xcd_remap", dict(H=192, K=4, V=128, n_pairs=200, n_solo=112, dtype="bf16", top_p=0.9,
+    # 2 x 8 tiles of 256 x 128: the XCD-aware order
+    ("mfma_xcd_remap", dict(H=192, K=4, V=256, n_pairs=100, n_solo=100, dtype="bf16", top_p=0.9,
                             cfg_w=2.5, steps=4)),
+    # at least 256 tiles of 256 x 256: the wide-tile kernel, ragged N and V % 4 != 0
+    ("mfma_wide_tiles", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, dtype="bf16",
+                             top_k=15, temperature=0.8, steps=10, shuffle=True)),
     ("mfma_text_rows", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=300,
                             dtype="bf16", top_k=5, steps=3, shuffle=True)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
