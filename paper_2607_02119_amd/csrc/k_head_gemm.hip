@@ -109,25 +109,22 @@ __global__ __launch_bounds__(256) void head_gemm_f32(HeadView hv, StepView sv) {
 
 }  // namespace
 
-hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t st) {
-  hipError_t e = hipSuccess;
+hipError_t launch_head_gemm_part(const HeadView &hv, const StepView &sv, bool text,
+                                 hipStream_t st) {
+  const int M = text ? sv.n_text : sv.Mg;
+  if (M == 0) return hipSuccess;
   if (hv.dtype == MCD_F32) {
-    if (sv.Mg > 0) {
-      hipLaunchKernelGGL(head_gemm_f32<false>, dim3((hv.N + 63) / 64), dim3(256), 0, st, hv, sv);
-      e = hipGetLastError();
-    }
-    if (e == hipSuccess && sv.n_text > 0) {
-      hipLaunchKernelGGL(head_gemm_f32<true>, dim3((hv.V_text + 63) / 64), dim3(256), 0, st, hv,
-                         sv);
-      e = hipGetLastError();
-    }
-    return e;
+    const int N = text ? hv.V_text : hv.N;
+    if (text) hipLaunchKernelGGL(head_gemm_f32<true>, dim3((N + 63) / 64), dim3(256), 0, st, hv, sv);
+    else hipLaunchKernelGGL(head_gemm_f32<false>, dim3((N + 63) / 64), dim3(256), 0, st, hv, sv);
+    return hipGetLastError();
   }
-  if (sv.Mg > 0)
-    e = sv.Mg <= 128 ? launch_stream_gemm(hv, sv, false, st) : launch_mfma_gemm(hv, sv, false, st);
-  if (e == hipSuccess && sv.n_text > 0)
-    e = sv.n_text <= 128 ? launch_stream_gemm(hv, sv, true, st)
-                         : launch_mfma_gemm(hv, sv, true, st);
+  return M <= 128 ? launch_stream_gemm(hv, sv, text, st) : launch_mfma_gemm(hv, sv, text, st);
+}
+
+hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t st) {
+  hipError_t e = launch_head_gemm_part(hv, sv, false, st);
+  if (e == hipSuccess) e = launch_head_gemm_part(hv, sv, true, st);
   return e;
 }
 

@@ -1,12 +1,14 @@
 // Host side of libmcd: argument validation, the batch plan and kernel launches.
 // Nothing here allocates device memory or synchronises, except
-// mcd_read_device_status.
+// mcd_read_device_status.  A head creates one extra stream and two events the
+// first time it runs a batch with both audio and text rows.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -16,6 +18,12 @@
 struct mcd_head {
   mcd::HeadView hv;
   int32_t max_delay;
+  // Batches with both audio and text rows run the two projections
+  // concurrently: the text part on a second stream of the head, forked from
+  // and joined back to the caller's stream with events (created on first use).
+  mutable std::mutex side_mu;
+  mutable hipStream_t side = nullptr;
+  mutable hipEvent_t fork = nullptr, join = nullptr;
 };
 
 namespace {
@@ -191,7 +199,13 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
   return MCD_OK;
 }
 
-void mcd_head_destroy(mcd_head *h) { delete h; }
+void mcd_head_destroy(mcd_head *h) {
+  if (!h) return;
+  if (h->fork) (void)hipEventDestroy(h->fork);
+  if (h->join) (void)hipEventDestroy(h->join);
+  if (h->side) (void)hipStreamDestroy(h->side);
+  delete h;
+}
 
 size_t mcd_plan_words(int32_t R) { return (size_t)mcd::kPlanHeader + (size_t)(R > 0 ? R : 0); }
 
@@ -270,12 +284,38 @@ size_t mcd_workspace_bytes(const mcd_head *h, int32_t R) {
   return (size_t)mcd::kStatusBytes + text_bytes(h, R > 0 ? R : 0);
 }
 
+namespace {
+
+// K1 for one batch.  Audio and text rows together: the audio projection on the
+// caller's stream and the text projection on the head's second stream, both
+// after everything already on the caller's stream, which waits for both.
+hipError_t run_head_gemm(const mcd_head *h, const mcd::StepView &sv, hipStream_t stream) {
+  if (h->hv.dtype != MCD_BF16 || sv.Mg == 0 || sv.n_text == 0)
+    return mcd::launch_head_gemm(h->hv, sv, stream);
+  std::lock_guard<std::mutex> lock(h->side_mu);
+  hipError_t e = hipSuccess;
+  if (!h->side) {
+    e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+  }
+  if ((e = hipEventRecord(h->fork, stream)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(h->side, h->fork, 0)) != hipSuccess) return e;
+  if ((e = mcd::launch_head_gemm_part(h->hv, sv, false, stream)) != hipSuccess) return e;
+  if ((e = mcd::launch_head_gemm_part(h->hv, sv, true, h->side)) != hipSuccess) return e;
+  if ((e = hipEventRecord(h->join, h->side)) != hipSuccess) return e;
+  return hipStreamWaitEvent(stream, h->join, 0);
+}
+
+}  // namespace
+
 mcd_status mcd_head_step(const mcd_head *h, const mcd_step_args *a, hipStream_t stream) {
   mcd::StepView sv;
   mcd_status s = make_step_view(h, a, true, sv);
   if (s != MCD_OK) return s;
   if (sv.R == 0) return MCD_OK;
-  hipError_t e = mcd::launch_head_gemm(h->hv, sv, stream);
+  hipError_t e = run_head_gemm(h, sv, stream);
   if (e != hipSuccess) return hip_fail(e, "head GEMM launch");
   e = mcd::launch_sample(h->hv, sv, true, stream);
   if (e != hipSuccess) return hip_fail(e, "sample launch");
@@ -287,7 +327,7 @@ mcd_status mcd_head_logits(const mcd_head *h, const mcd_step_args *a, hipStream_
   mcd_status s = make_step_view(h, a, true, sv);
   if (s != MCD_OK) return s;
   if (sv.R == 0) return MCD_OK;
-  hipError_t e = mcd::launch_head_gemm(h->hv, sv, stream);
+  hipError_t e = run_head_gemm(h, sv, stream);
   return e == hipSuccess ? MCD_OK : hip_fail(e, "head GEMM launch");
 }
 

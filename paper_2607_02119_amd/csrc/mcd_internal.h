@@ -64,6 +64,9 @@ inline int32_t text_parts_for(int32_t V_text) {
 
 // Kernel launchers (one .hip file each).
 hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t stream);
+// one part of it: the audio rows, or the text rows when text is set
+hipError_t launch_head_gemm_part(const HeadView &hv, const StepView &sv, bool text,
+                                 hipStream_t stream);
 // bf16 projection kernels (audio rows, or the text rows when text is set)
 hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
                               hipStream_t stream);   // at most 128 GEMM rows
