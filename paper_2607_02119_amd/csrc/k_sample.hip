@@ -38,10 +38,8 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
 constexpr int kBins = 512;          // bins of width 1/16 below the maximum, plus one open bin
 constexpr float kBinScale = 16.0f;
-constexpr int kCap = 256;           // largest cut bin ranked directly
 
 __device__ inline uint32_t order_key(float x) {
   if (x == 0.0f) x = 0.0f;  // -0 and +0 compare equal
@@ -60,7 +58,6 @@ __device__ inline bool plan_ok(const StepView &sv) {
 }
 
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
-__device__ inline int wave_id() { return threadIdx.x / kWave; }
 
 template <typename T>
 __device__ inline void keep_better(T &bv, int &bi, T v, int i) {
@@ -156,29 +153,28 @@ __device__ __forceinline__ void wave_argmax_f64(double &bv, int &bi) {
   bi = __builtin_amdgcn_readlane(bi, 63);
 }
 
-// ---- workgroup shared memory and reductions ----------------------------------
-template <int GPT>
-struct Smem {
-  uint32_t cnt[kBins + 1];               // top-k bin counts
-  unsigned long long mh[kBins + 1];      // top-p bin masses
-  // elements of the cut bin, and their exact ranks
-  struct Entry {
-    float v;
-    int id;
-  };
-  Entry le[kCap];
-  unsigned long long lm[kCap];           // their masses (top-p)
-  int lr[kCap];
-  unsigned long long lsm[kCap];          // masses in rank order, then the mass before each rank
-  uint32_t keepbits[kThreads];           // kept cut-bin elements, one bit per slot of a thread
-  uint32_t lcount;
-  // block reductions (two slots, alternating, one barrier each)
-  uint32_t ru[2][kWaves];
-  unsigned long long r64[2][kWaves];
-  double rd[2][kWaves];
-  int ri[2][kWaves];
-  // radix select (fallback); reused for the draw list once the selection is done
-  unsigned long long hist[3][256];
+// ---- vector groups -------------------------------------------------------------
+// A vector is handled by a group of TPV threads: one wave (TPV = 64, several
+// vectors per workgroup, no workgroup barriers at all) or the whole 256-thread
+// workgroup.  Group barriers and reductions follow the group.
+template <int TPV>
+struct Grp {
+  static_assert(TPV == kWave || TPV == kThreads, "a wave or the workgroup");
+  static constexpr int kGW = TPV / kWave;       // waves per group
+  __device__ static int tid() { return (int)threadIdx.x % TPV; }
+  __device__ static int wave() { return tid() / kWave; }
+  __device__ static int index() { return (int)threadIdx.x / TPV; }
+  __device__ static void sync() {
+    if constexpr (TPV == kWave) {
+      // one wave: its LDS accesses complete in program order; keep the
+      // compiler from moving any across this point
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    } else {
+      __syncthreads();
+    }
+  }
 };
 
 // A group of four ids with kept members, moved to the thread that draws it.
@@ -187,57 +183,88 @@ struct DrawItem {
   uint32_t bits;
   float x[4];
 };
-constexpr int kDrawCap = 256;
-static_assert(kDrawCap * sizeof(DrawItem) <= 3 * 256 * sizeof(unsigned long long), "draw list fits");
 
-template <int GPT>
-__device__ __forceinline__ uint32_t block_max_u32(uint32_t x, Smem<GPT> &sm, int &slot) {
+template <int TPV>
+struct Smem {
+  struct Entry {
+    float v;
+    int id;
+  };
+  uint32_t cnt[kBins + 1];               // top-k bin counts
+  union {
+    unsigned long long mh[kBins + 1];    // top-p bin masses
+    unsigned long long hist[3][256];     // radix select (fallback)
+    DrawItem draw[TPV];                  // kept groups, once the selection is done
+  } u;
+  // elements of the cut bin (at most TPV), and their exact ranks
+  Entry le[TPV];
+  unsigned long long lm[TPV];            // their masses (top-p)
+  int lr[TPV];
+  unsigned long long lsm[TPV];           // masses in rank order, then the mass before each rank
+  uint32_t keepbits[TPV];                // kept cut-bin elements, one bit per slot of a thread
+  uint32_t lcount;
+  // reductions across the waves of a group (two slots, alternating, one barrier each)
+  uint32_t ru[2][Grp<TPV>::kGW];
+  unsigned long long r64[2][Grp<TPV>::kGW];
+  double rd[2][Grp<TPV>::kGW];
+  int ri[2][Grp<TPV>::kGW];
+};
+
+template <int TPV>
+__device__ __forceinline__ uint32_t grp_max_u32(uint32_t x, Smem<TPV> &sm, int &slot) {
   x = wave_max_u32(x);
-  if (lane_id() == 0) sm.ru[slot][wave_id()] = x;
-  __syncthreads();
+  if constexpr (TPV == kWave) return x;
+  if (lane_id() == 0) sm.ru[slot][Grp<TPV>::wave()] = x;
+  Grp<TPV>::sync();
   uint32_t r = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = sm.ru[slot][w] > r ? sm.ru[slot][w] : r;
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) r = sm.ru[slot][w] > r ? sm.ru[slot][w] : r;
   slot ^= 1;
   return r;
 }
 
-template <int GPT>
-__device__ __forceinline__ uint32_t block_min_u32(uint32_t x, Smem<GPT> &sm, int &slot) {
+template <int TPV>
+__device__ __forceinline__ uint32_t grp_min_u32(uint32_t x, Smem<TPV> &sm, int &slot) {
   x = wave_min_u32(x);
-  if (lane_id() == 0) sm.ru[slot][wave_id()] = x;
-  __syncthreads();
+  if constexpr (TPV == kWave) return x;
+  if (lane_id() == 0) sm.ru[slot][Grp<TPV>::wave()] = x;
+  Grp<TPV>::sync();
   uint32_t r = 0xFFFFFFFFu;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = sm.ru[slot][w] < r ? sm.ru[slot][w] : r;
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) r = sm.ru[slot][w] < r ? sm.ru[slot][w] : r;
   slot ^= 1;
   return r;
 }
 
-template <int GPT>
-__device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, Smem<GPT> &sm, int &slot) {
+template <int TPV>
+__device__ __forceinline__ uint64_t grp_sum_u64(uint64_t x, Smem<TPV> &sm, int &slot) {
   x = readlane_u64(wave_incl_add_u64(x), 63);
-  if (lane_id() == 0) sm.r64[slot][wave_id()] = x;
-  __syncthreads();
+  if constexpr (TPV == kWave) return x;
+  if (lane_id() == 0) sm.r64[slot][Grp<TPV>::wave()] = x;
+  Grp<TPV>::sync();
   uint64_t r = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) r += sm.r64[slot][w];
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) r += sm.r64[slot][w];
   slot ^= 1;
   return r;
 }
 
-// exclusive prefix of x over the threads in id order, and the block total
-template <int GPT>
-__device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t &total,
-                                                        Smem<GPT> &sm, int &slot) {
+// exclusive prefix of x over the group's threads in order, and the total
+template <int TPV>
+__device__ __forceinline__ uint32_t grp_excl_scan_u32(uint32_t x, uint32_t &total, Smem<TPV> &sm,
+                                                      int &slot) {
   const uint32_t incl = wave_incl_add_u32(x);
-  if (lane_id() == 63) sm.ru[slot][wave_id()] = incl;
-  __syncthreads();
+  if constexpr (TPV == kWave) {
+    total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    return incl - x;
+  }
+  if (lane_id() == 63) sm.ru[slot][Grp<TPV>::wave()] = incl;
+  Grp<TPV>::sync();
   uint32_t before = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) {
     const uint32_t c = sm.ru[slot][w];
-    if (w < wave_id()) before += c;
+    if (w < Grp<TPV>::wave()) before += c;
     tot += c;
   }
   slot ^= 1;
@@ -245,48 +272,51 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t &to
   return before + incl - x;
 }
 
-// inclusive prefix of x over the threads in id order
-template <int GPT>
-__device__ __forceinline__ uint64_t block_incl_scan_u64(uint64_t x, Smem<GPT> &sm, int &slot) {
+// inclusive prefix of x over the group's threads in order
+template <int TPV>
+__device__ __forceinline__ uint64_t grp_incl_scan_u64(uint64_t x, Smem<TPV> &sm, int &slot) {
   const uint64_t incl = wave_incl_add_u64(x);
-  if (lane_id() == 63) sm.r64[slot][wave_id()] = incl;
-  __syncthreads();
+  if constexpr (TPV == kWave) return incl;
+  if (lane_id() == 63) sm.r64[slot][Grp<TPV>::wave()] = incl;
+  Grp<TPV>::sync();
   uint64_t before = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w)
-    if (w < wave_id()) before += sm.r64[slot][w];
+  for (int w = 0; w < Grp<TPV>::kGW; ++w)
+    if (w < Grp<TPV>::wave()) before += sm.r64[slot][w];
   slot ^= 1;
   return before + incl;
 }
 
-template <int GPT>
-__device__ __forceinline__ int block_argmax_f32(float bv, int bi, Smem<GPT> &sm, int &slot) {
+template <int TPV>
+__device__ __forceinline__ int grp_argmax_f32(float bv, int bi, Smem<TPV> &sm, int &slot) {
   wave_argmax_f32(bv, bi);
+  if constexpr (TPV == kWave) return bi;
   if (lane_id() == 0) {
-    sm.rd[slot][wave_id()] = (double)bv;
-    sm.ri[slot][wave_id()] = bi;
+    sm.rd[slot][Grp<TPV>::wave()] = (double)bv;
+    sm.ri[slot][Grp<TPV>::wave()] = bi;
   }
-  __syncthreads();
+  Grp<TPV>::sync();
   double rv = sm.rd[slot][0];
   int ri = sm.ri[slot][0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
+  for (int w = 1; w < Grp<TPV>::kGW; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
   slot ^= 1;
   return ri;
 }
 
-template <int GPT>
-__device__ __forceinline__ int block_argmax_f64(double bv, int bi, Smem<GPT> &sm, int &slot) {
+template <int TPV>
+__device__ __forceinline__ int grp_argmax_f64(double bv, int bi, Smem<TPV> &sm, int &slot) {
   wave_argmax_f64(bv, bi);
+  if constexpr (TPV == kWave) return bi;
   if (lane_id() == 0) {
-    sm.rd[slot][wave_id()] = bv;
-    sm.ri[slot][wave_id()] = bi;
+    sm.rd[slot][Grp<TPV>::wave()] = bv;
+    sm.ri[slot][Grp<TPV>::wave()] = bi;
   }
-  __syncthreads();
+  Grp<TPV>::sync();
   double rv = sm.rd[slot][0];
   int ri = sm.ri[slot][0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
+  for (int w = 1; w < Grp<TPV>::kGW; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
   slot ^= 1;
   return ri;
 }
@@ -340,15 +370,16 @@ struct Cut {
 // `pass` counts the digit passes done so far in this vector and selects the
 // rotating buffers; the buffers pass % 3 and (pass + 1) % 3 must be zero on
 // entry, and the two after the last one used are zero again on exit.
-template <int GPT, bool MASS>
-__device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t active, const uint64_t *mass,
-                            uint64_t target, Smem<GPT> &sm, int &pass) {
+template <int GPT, int TPV, bool MASS>
+__device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t active,
+                                            const uint64_t *mass, uint64_t target,
+                                            Smem<TPV> &sm, int &pass) {
   constexpr int EPL = 4 * GPT;
-  const int tid = threadIdx.x, lane = lane_id();
+  const int gt = Grp<TPV>::tid(), lane = lane_id();
   uint32_t prefix = 0, pmask = 0;
   uint64_t rem = target;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    unsigned long long *h = sm.hist[pass % 3];
+    unsigned long long *h = sm.u.hist[pass % 3];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
       const uint32_t key = order_key(x[i]);
@@ -357,7 +388,7 @@ __device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t 
         atomicAdd(&h[d], MASS ? (unsigned long long)mass[i] : 1ull);
       }
     }
-    __syncthreads();
+    Grp<TPV>::sync();
     // every wave scans all 256 digits (lane l: digits 255-4l .. 252-4l)
     uint64_t v[4], lsum = 0;
 #pragma unroll
@@ -368,7 +399,7 @@ __device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t 
     const uint64_t incl = wave_incl_add_u64(lsum);
     const uint64_t excl = incl - lsum;
     // clear the buffer of the pass after next (its last readers passed the barrier above)
-    sm.hist[(pass + 2) % 3][tid] = 0;
+    for (int b = gt; b < 256; b += TPV) sm.u.hist[(pass + 2) % 3][b] = 0;
     ++pass;
     const uint64_t bal = __ballot(excl < rem && incl >= rem);
     if (bal == 0) return Cut{0u, false, 0, true};
@@ -399,10 +430,11 @@ __device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t 
 
 // Apply a cut to the active set.  For an exact cut with fewer than all of the
 // ties at kappa wanted, the `need_n` lowest ids among the ties are kept (id of
-// slot 4q + j of thread tid: 4 (q * 256 + tid) + j).
-template <int GPT>
-__device__ __forceinline__ uint32_t apply_cut(const float (&x)[4 * GPT], uint32_t active, const Cut &c,
-                              uint64_t need_n, Smem<GPT> &sm, int &slot) {
+// slot 4q + j of group thread t: 4 (q * TPV + t) + j).
+template <int GPT, int TPV>
+__device__ __forceinline__ uint32_t apply_cut(const float (&x)[4 * GPT], uint32_t active,
+                                              const Cut &c, uint64_t need_n, Smem<TPV> &sm,
+                                              int &slot) {
   constexpr int EPL = 4 * GPT;
   if (c.all) return active;
   uint32_t keep = 0, ties = 0;
@@ -419,7 +451,7 @@ __device__ __forceinline__ uint32_t apply_cut(const float (&x)[4 * GPT], uint32_
   for (int q = 0; q < GPT; ++q) {
     const uint32_t tq = (ties >> (4 * q)) & 0xFu;
     uint32_t total;
-    const uint32_t before = block_excl_scan_u32((uint32_t)__popc(tq), total, sm, slot);
+    const uint32_t before = grp_excl_scan_u32<TPV>((uint32_t)__popc(tq), total, sm, slot);
     uint64_t rank = base + before;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -483,11 +515,25 @@ __device__ __forceinline__ void bins_of(const float (&x)[4 * GPT], uint32_t acti
   }
 }
 
-// Rank the listed elements of a cut bin by (score desc, id asc); n <= kCap.
-template <int GPT>
-__device__ __forceinline__ void rank_list(Smem<GPT> &sm, int n) {
-  using Entry = typename Smem<GPT>::Entry;
-  const int t = threadIdx.x;
+// id of register slot i of group thread t
+template <int TPV>
+__device__ __forceinline__ int id_of(int i, int t) {
+  return 4 * ((i / 4) * TPV + t) + (i % 4);
+}
+
+// Group thread that owns id e, and the slot of e in its registers.
+template <int TPV>
+__device__ __forceinline__ void owner_of(int e, int &thread, int &slot) {
+  const int g = e >> 2;
+  thread = g % TPV;
+  slot = 4 * (g / TPV) + (e & 3);
+}
+
+// Rank the listed elements of a cut bin by (score desc, id asc); n <= TPV.
+template <int TPV>
+__device__ __forceinline__ void rank_list(Smem<TPV> &sm, int n) {
+  using Entry = typename Smem<TPV>::Entry;
+  const int t = Grp<TPV>::tid();
   if (t < n) {
     const Entry me = sm.le[t];
     auto ahead = [&](const Entry &o) __attribute__((always_inline)) {
@@ -503,25 +549,28 @@ __device__ __forceinline__ void rank_list(Smem<GPT> &sm, int n) {
   }
 }
 
-// Thread that owns id e, and the slot of e in its registers.
-__device__ __forceinline__ void owner_of(int e, int &thread, int &slot) {
-  const int g = e >> 2;
-  thread = g % kThreads;
-  slot = 4 * (g / kThreads) + (e & 3);
+// The radix buffers alias the top-p histogram: wait for its last readers.
+template <int TPV>
+__device__ __forceinline__ void zero_radix(Smem<TPV> &sm) {
+  Grp<TPV>::sync();
+  for (int b = Grp<TPV>::tid(); b < 2 * 256; b += TPV) sm.u.hist[b / 256][b % 256] = 0;
+  Grp<TPV>::sync();
 }
 
-template <int GPT>
-__device__ __forceinline__ uint32_t radix_topk(const float (&x)[4 * GPT], uint32_t active, int top_k,
-                                            Smem<GPT> &sm, int &slot, int &pass) {
-  const Cut c = radix_select<GPT, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
-  return apply_cut<GPT>(x, active, c, c.need, sm, slot);
+template <int GPT, int TPV>
+__device__ __forceinline__ uint32_t radix_topk(const float (&x)[4 * GPT], uint32_t active,
+                                               int top_k, Smem<TPV> &sm, int &slot, int &pass) {
+  zero_radix(sm);
+  const Cut c = radix_select<GPT, TPV, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
+  return apply_cut<GPT, TPV>(x, active, c, c.need, sm, slot);
 }
 
-template <int GPT>
+template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t radix_topp(const float (&x)[4 * GPT], uint32_t active,
-                                            const uint64_t (&mass)[4 * GPT], uint64_t target,
-                                            Smem<GPT> &sm, int &slot, int &pass) {
-  const Cut c = radix_select<GPT, true>(x, active, mass, target, sm, pass);
+                                               const uint64_t (&mass)[4 * GPT], uint64_t target,
+                                               Smem<TPV> &sm, int &slot, int &pass) {
+  zero_radix(sm);
+  const Cut c = radix_select<GPT, TPV, true>(x, active, mass, target, sm, pass);
   uint64_t need_n = 0;
   if (c.exact) {
     // every element tied at kappa carries the same mass q: the fewest reaching rem
@@ -530,33 +579,27 @@ __device__ __forceinline__ uint32_t radix_topp(const float (&x)[4 * GPT], uint32
     for (int i = 0; i < 4 * GPT; ++i)
       if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass[i];
     // every nonzero q is the same value, so the halves reduce independently
-    const uint64_t qhi = block_max_u32((uint32_t)(q >> 32), sm, slot);
-    const uint64_t qlo = block_max_u32((uint32_t)q, sm, slot);
+    const uint64_t qhi = grp_max_u32<TPV>((uint32_t)(q >> 32), sm, slot);
+    const uint64_t qlo = grp_max_u32<TPV>((uint32_t)q, sm, slot);
     q = qhi << 32 | qlo;
     need_n = q ? (c.need + q - 1) / q : 1;
   }
-  return apply_cut<GPT>(x, active, c, need_n, sm, slot);
-}
-
-template <int GPT>
-__device__ __forceinline__ void zero_radix(Smem<GPT> &sm) {
-#pragma unroll
-  for (int b = 0; b < 2; ++b) sm.hist[b][threadIdx.x] = 0;
-  __syncthreads();
+  return apply_cut<GPT, TPV>(x, active, c, need_n, sm, slot);
 }
 
 // top-k over the active set; `mx` is the maximum active score
-template <int GPT>
+template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint32_t active,
-                                                float mx, int top_k, Smem<GPT> &sm, int &slot,
+                                                float mx, int top_k, Smem<TPV> &sm, int &slot,
                                                 int &pass, int V) {
   constexpr int EPL = 4 * GPT;
+  const int gt = Grp<TPV>::tid();
   int bin[EPL];
   bins_of<GPT>(x, active, mx, bin);
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
     if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.cnt[bin[i]], 1u);
-  __syncthreads();
+  Grp<TPV>::sync();
   uint64_t above, inbin;
   const int bc = find_cut_bin(sm.cnt, (uint64_t)top_k, above, inbin, (uint64_t)V);
   const uint64_t need = (uint64_t)top_k - above;
@@ -567,28 +610,25 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
       if (bin[i] >= 0 && bin[i] <= bc) keep |= 1u << i;
     return keep;
   }
-  if (bc == kBins || inbin > (uint64_t)kCap) {
-    zero_radix(sm);
-    return radix_topk<GPT>(x, active, top_k, sm, slot, pass);
-  }
+  if (bc == kBins || inbin > (uint64_t)TPV) return radix_topk<GPT, TPV>(x, active, top_k, sm, slot, pass);
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     if (bin[i] == bc) {
       const int s = (int)atomicAdd(&sm.lcount, 1u);
-      sm.le[s] = {x[i], 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4)};
+      sm.le[s] = {x[i], id_of<TPV>(i, gt)};
     }
   }
-  __syncthreads();
+  Grp<TPV>::sync();
   rank_list(sm, (int)inbin);
-  if ((int)threadIdx.x < (int)inbin && (uint64_t)sm.lr[threadIdx.x] < need) {
+  if (gt < (int)inbin && (uint64_t)sm.lr[gt] < need) {
     int ow, sl;
-    owner_of(sm.le[threadIdx.x].id, ow, sl);
+    owner_of<TPV>(sm.le[gt].id, ow, sl);
     atomicOr(&sm.keepbits[ow], 1u << sl);
   }
-  __syncthreads();
-  keep = sm.keepbits[threadIdx.x];
-  sm.keepbits[threadIdx.x] = 0;          // next use follows at least one barrier
-  if (threadIdx.x == 0) sm.lcount = 0;
+  Grp<TPV>::sync();
+  keep = sm.keepbits[gt];
+  sm.keepbits[gt] = 0;          // next use follows at least one group barrier
+  if (gt == 0) sm.lcount = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
     if (bin[i] >= 0 && bin[i] < bc) keep |= 1u << i;
@@ -596,11 +636,12 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
 }
 
 // top-p over the active set (the survivors of top-k); `mx` is their maximum
-template <int GPT>
+template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint32_t active,
-                                                float mx, float top_p, Smem<GPT> &sm, int &slot,
+                                                float mx, float top_p, Smem<TPV> &sm, int &slot,
                                                 int &pass) {
   constexpr int EPL = 4 * GPT;
+  const int gt = Grp<TPV>::tid();
   // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
   // converted exactly to a 64-bit integer
   uint64_t mass[EPL];
@@ -610,72 +651,74 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
     mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
     zl += mass[i];
   }
-  const uint64_t Z = block_sum_u64(zl, sm, slot);
+  // the mass histogram shares its storage with the radix buffers, which top-k
+  // may have used: clear it once their last readers are past
+  Grp<TPV>::sync();
+  for (int b = gt; b <= kBins; b += TPV) sm.u.mh[b] = 0;
+  const uint64_t Z = grp_sum_u64<TPV>(zl, sm, slot);
   uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
   if (target < 1) target = 1;
   if (target > Z) return active;
   int bin[EPL];
   bins_of<GPT>(x, active, mx, bin);
+  if constexpr (TPV == kWave) Grp<TPV>::sync();   // the clearing stores before the adds
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.mh[bin[i]], (unsigned long long)mass[i]);
-  __syncthreads();
+    if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.u.mh[bin[i]], (unsigned long long)mass[i]);
+  Grp<TPV>::sync();
   uint64_t above, inbin;
-  const int bc = find_cut_bin(sm.mh, target, above, inbin, Z);
-  if (bc == kBins) {
-    zero_radix(sm);
-    return radix_topp<GPT>(x, active, mass, target, sm, slot, pass);
-  }
+  const int bc = find_cut_bin(sm.u.mh, target, above, inbin, Z);
+  if (bc == kBins) return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     if (bin[i] == bc) {
       const int s = (int)atomicAdd(&sm.lcount, 1u);
-      if (s < kCap) {
-        sm.le[s] = {x[i], 4 * ((i / 4) * kThreads + (int)threadIdx.x) + (i % 4)};
+      if (s < TPV) {
+        sm.le[s] = {x[i], id_of<TPV>(i, gt)};
         sm.lm[s] = mass[i];
       }
     }
   }
-  __syncthreads();
+  Grp<TPV>::sync();
   const int n = (int)sm.lcount;
-  if (n > kCap) {
-    __syncthreads();   // everyone has read lcount
-    if (threadIdx.x == 0) sm.lcount = 0;
-    zero_radix(sm);
-    return radix_topp<GPT>(x, active, mass, target, sm, slot, pass);
+  if (n > TPV) {
+    Grp<TPV>::sync();   // everyone has read lcount
+    if (gt == 0) sm.lcount = 0;
+    return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
   }
   rank_list(sm, n);
-  __syncthreads();
-  if ((int)threadIdx.x < n) sm.lsm[sm.lr[threadIdx.x]] = sm.lm[threadIdx.x];
-  __syncthreads();
-  // mass of the ranks before each rank: a block scan (thread r holds rank r)
-  const uint64_t mr = (int)threadIdx.x < n ? sm.lsm[threadIdx.x] : 0;
-  const uint64_t incl = block_incl_scan_u64(mr, sm, slot);
-  if ((int)threadIdx.x < n) sm.lsm[threadIdx.x] = incl - mr;   // every read of lsm is done
-  __syncthreads();
+  Grp<TPV>::sync();
+  if (gt < n) sm.lsm[sm.lr[gt]] = sm.lm[gt];
+  Grp<TPV>::sync();
+  // mass of the ranks before each rank: a group scan (thread r holds rank r)
+  const uint64_t mr = gt < n ? sm.lsm[gt] : 0;
+  const uint64_t incl = grp_incl_scan_u64<TPV>(mr, sm, slot);
+  if constexpr (TPV == kWave) Grp<TPV>::sync();   // every read of lsm before the writes
+  if (gt < n) sm.lsm[gt] = incl - mr;
+  Grp<TPV>::sync();
   // entry kept iff the mass strictly before it (in rank order) is below target
-  if ((int)threadIdx.x < n && above + sm.lsm[sm.lr[threadIdx.x]] < target) {
+  if (gt < n && above + sm.lsm[sm.lr[gt]] < target) {
     int ow, sl;
-    owner_of(sm.le[threadIdx.x].id, ow, sl);
+    owner_of<TPV>(sm.le[gt].id, ow, sl);
     atomicOr(&sm.keepbits[ow], 1u << sl);
   }
-  __syncthreads();
-  uint32_t keep = sm.keepbits[threadIdx.x];
-  sm.keepbits[threadIdx.x] = 0;
-  if (threadIdx.x == 0) sm.lcount = 0;
+  Grp<TPV>::sync();
+  uint32_t keep = sm.keepbits[gt];
+  sm.keepbits[gt] = 0;
+  if (gt == 0) sm.lcount = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
     if (bin[i] >= 0 && bin[i] < bc) keep |= 1u << i;
   return keep;
 }
 
-template <int GPT>
+template <int GPT, int TPV>
 __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
                                                uint32_t active, int V, bool greedy, int top_k,
                                                float top_p, uint64_t rkey, int t, int k,
-                                               Smem<GPT> &sm, int &slot) {
+                                               Smem<TPV> &sm, int &slot) {
   constexpr int EPL = 4 * GPT;
-  const int tid = threadIdx.x;
+  const int gt = Grp<TPV>::tid();
   uint32_t mk = 0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
@@ -683,55 +726,60 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
       const uint32_t key = order_key(x[i]);
       mk = key > mk ? key : mk;
     }
-  mk = block_max_u32(mk, sm, slot);   // also publishes the zeroed histograms
+  // also publishes the cleared count histogram (one barrier for a workgroup group)
+  mk = grp_max_u32<TPV>(mk, sm, slot);
+  if constexpr (TPV == kWave) Grp<TPV>::sync();
   if (greedy) {
     uint32_t id = 0xFFFFFFFFu;
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if (((active >> i) & 1) && order_key(x[i]) == mk) {
-        const uint32_t e = 4u * (uint32_t)((i / 4) * kThreads + tid) + (uint32_t)(i % 4);
+        const uint32_t e = (uint32_t)id_of<TPV>(i, gt);
         id = e < id ? e : id;
       }
-    return (int)block_min_u32(id, sm, slot);
+    return (int)grp_min_u32<TPV>(id, sm, slot);
   }
   const float mx = key_to_float(mk);
   int pass = 0;
   uint32_t kept = active;
-  if (top_k > 0 && top_k < V) kept = select_topk<GPT>(x, kept, mx, top_k, sm, slot, pass, V);
-  if (top_p < 1.0f) kept = select_topp<GPT>(x, kept, mx, top_p, sm, slot, pass);
-  // Gumbel-max over the kept ids, one Philox block per group with a kept id
+  if (top_k > 0 && top_k < V) kept = select_topk<GPT, TPV>(x, kept, mx, top_k, sm, slot, pass, V);
+  if (top_p < 1.0f) kept = select_topp<GPT, TPV>(x, kept, mx, top_p, sm, slot, pass);
+  // Gumbel-max over the kept ids, one Philox block per group of four ids
   double bv = -INFINITY;
   int bi = INT32_MAX;
-  if (top_k > 0 && top_k <= kDrawCap) {
+  if (top_k > 0 && top_k <= TPV) {
     // few kept groups: move them to one thread each, so that no wave runs
     // several Philox blocks one after another
     uint32_t n = 0;
 #pragma unroll
     for (int q = 0; q < GPT; ++q) n += ((kept >> (4 * q)) & 0xFu) ? 1u : 0u;
     uint32_t total;
-    uint32_t pos = block_excl_scan_u32(n, total, sm, slot);
-    DrawItem *dl = reinterpret_cast<DrawItem *>(&sm.hist[0][0]);
+    uint32_t pos = grp_excl_scan_u32<TPV>(n, total, sm, slot);
+    // the draw list shares its storage with the top-p histogram and the radix
+    // buffers: wait for their last readers
+    if constexpr (TPV == kWave) Grp<TPV>::sync();
+    DrawItem *dl = sm.u.draw;
 #pragma unroll
     for (int q = 0; q < GPT; ++q) {
       const uint32_t bits = (kept >> (4 * q)) & 0xFu;
-      if (bits) dl[pos++] = {q * kThreads + tid, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
+      if (bits) dl[pos++] = {q * TPV + gt, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
     }
-    __syncthreads();
-    if (tid < (int)total) {
-      const DrawItem it = dl[tid];
+    Grp<TPV>::sync();
+    if (gt < (int)total) {
+      const DrawItem it = dl[gt];
       const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)it.g);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if ((it.bits >> j) & 1)
           keep_better(bv, bi, (double)it.x[j] + (double)gumbel_from_word(w.w[j]), 4 * it.g + j);
     }
-    return block_argmax_f64(bv, bi, sm, slot);
+    return grp_argmax_f64<TPV>(bv, bi, sm, slot);
   }
 #pragma unroll
   for (int q = 0; q < GPT; ++q) {
     const uint32_t bits = (kept >> (4 * q)) & 0xFu;
     if (bits) {
-      const int g = q * kThreads + tid;
+      const int g = q * TPV + gt;
       const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -739,24 +787,25 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
           keep_better(bv, bi, (double)x[4 * q + j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
     }
   }
-  return block_argmax_f64(bv, bi, sm, slot);
+  return grp_argmax_f64<TPV>(bv, bi, sm, slot);
 }
 
-template <int GPT>
+// One vector per group of TPV threads: 256 / TPV vectors per workgroup.
+template <int GPT, int TPV>
 __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView sv,
                                                           int with_text) {
   constexpr int EPL = 4 * GPT;
-  __shared__ Smem<GPT> sm;
-  const int tid = threadIdx.x;
-  const int vec = blockIdx.x;
+  constexpr int G = kThreads / TPV;
+  __shared__ Smem<TPV> smem[G];
+  Smem<TPV> &sm = smem[Grp<TPV>::index()];
+  const int gt = Grp<TPV>::tid();
+  const int vec = (int)blockIdx.x * G + Grp<TPV>::index();
   const int n_audio = sv.Rs * hv.K;
-  // histograms start at zero (published by the first block reduction)
-  for (int b = tid; b <= kBins; b += kThreads) {
-    sm.cnt[b] = 0;
-    sm.mh[b] = 0;
-  }
-  sm.keepbits[tid] = 0;
-  if (tid == 0) sm.lcount = 0;
+  if (vec >= n_audio + (with_text ? sv.n_text : 0)) return;   // a whole group
+  // the count histogram starts at zero (published by the first group reduction)
+  for (int b = gt; b <= kBins; b += TPV) sm.cnt[b] = 0;
+  sm.keepbits[gt] = 0;
+  if (gt == 0) sm.lcount = 0;
   int slot = 0;
 
   // The scores depend only on the vector index: load them before anything
@@ -770,7 +819,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     if ((V & 3) == 0) {
 #pragma unroll
       for (int q = 0; q < GPT; ++q) {
-        const int g = q * kThreads + tid;
+        const int g = q * TPV + gt;
         float4 v = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         if (4 * g < V) v = *reinterpret_cast<const float4 *>(sc + 4 * g);
         x[4 * q + 0] = v.x;
@@ -781,38 +830,35 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     } else {
 #pragma unroll
       for (int i = 0; i < EPL; ++i) {
-        const int e = 4 * ((i / 4) * kThreads + tid) + (i % 4);
+        const int e = id_of<TPV>(i, gt);
         x[i] = e < V ? sc[e] : -INFINITY;
       }
     }
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const int e = 4 * ((i / 4) * kThreads + tid) + (i % 4);
-      if (e < V) active |= 1u << i;
-    }
+    for (int i = 0; i < EPL; ++i)
+      if (id_of<TPV>(i, gt) < V) active |= 1u << i;
   }
 
   if (!plan_ok(sv)) {
-    if (vec == 0 && tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    if (vec == 0 && gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
     return;
   }
   const int32_t *rows = sv.plan + kPlanHeader;
   if (vec >= n_audio) {
     // text row: reduce the (max, lowest argmax) partials of the text GEMM
     const int j = vec - n_audio;
-    if (!with_text || j >= sv.n_text) return;
     const int r = rows[sv.Mg + j];
     if (r < 0 || r >= sv.R) {
-      if (tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+      if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
       return;
     }
     float bv = -INFINITY;
     int bi = INT32_MAX;
-    for (int p = tid; p < sv.text_parts; p += kThreads)
+    for (int p = gt; p < sv.text_parts; p += TPV)
       keep_better(bv, bi, sv.text_val[(size_t)j * sv.text_parts + p],
                   sv.text_idx[(size_t)j * sv.text_parts + p]);
-    const int tok = block_argmax_f32(bv, bi, sm, slot);
-    for (int k = tid; k < hv.K; k += kThreads)
+    const int tok = grp_argmax_f32<TPV>(bv, bi, sm, slot);
+    for (int k = gt; k < hv.K; k += TPV)
       sv.tokens_out[(size_t)r * hv.K + k] = (k == 0) ? tok : hv.pad_id;
     return;
   }
@@ -821,7 +867,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
   const int r = paired ? rows[2 * s] : rows[2 * sv.n_pairs + (s - sv.n_pairs)];
   const int u = paired ? rows[2 * s + 1] : -1;
   if (r < 0 || r >= sv.R || u >= sv.R) {
-    if (tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
     return;
   }
   const int t = sv.step[r];
@@ -835,15 +881,15 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     const bool bad = !(T >= 0.0f) || isinf(T) || !(P > 0.0f) ||
                      (paired && !isfinite(sv.cfg_w[r]));
     if (bad) {
-      if (tid == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
+      if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
       const uint64_t rkey = sv.rng_key ? sv.rng_key[r] : (uint64_t)r;
-      token = select_and_draw<GPT>(sv, x, active, V, T == 0.0f, sv.top_k[r], P, rkey, t, k, sm,
-                                   slot);
+      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, sv.top_k[r], P, rkey, t, k,
+                                        sm, slot);
       sampled = true;
     }
   }
-  if (tid == 0) {
+  if (gt == 0) {
     sv.tokens_out[(size_t)r * hv.K + k] = token;
     if (u >= 0) sv.tokens_out[(size_t)u * hv.K + k] = token;
     const int gslot = sv.grid_slot[r];
@@ -856,24 +902,35 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
   }
 }
 
-template <int GPT>
-hipError_t launch_gpt(const HeadView &hv, const StepView &sv, int nblk, bool with_text,
+template <int GPT, int TPV>
+hipError_t launch_gpt(const HeadView &hv, const StepView &sv, int nvec, bool with_text,
                       hipStream_t st) {
-  hipLaunchKernelGGL(sample_kernel<GPT>, dim3(nblk), dim3(kThreads), 0, st, hv, sv,
-                     (int)with_text);
+  constexpr int G = kThreads / TPV;
+  hipLaunchKernelGGL((sample_kernel<GPT, TPV>), dim3((nvec + G - 1) / G), dim3(kThreads), 0, st,
+                     hv, sv, (int)with_text);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// One wave per vector when there are many vectors of at most 1024 ids (more
+// vectors in flight per compute unit, no workgroup barriers); one workgroup per
+// vector otherwise (shorter latency per vector).
+constexpr int kWaveVectorsMin = 1024;
+
 hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t st) {
-  const int nblk = sv.Rs * hv.K + (with_text ? sv.n_text : 0);
-  if (nblk == 0) return hipSuccess;
+  const int nvec = sv.Rs * hv.K + (with_text ? sv.n_text : 0);
+  if (nvec == 0) return hipSuccess;
   const int groups = (hv.V + 3) / 4;
-  if (groups <= kThreads) return launch_gpt<1>(hv, sv, nblk, with_text, st);
-  if (groups <= 2 * kThreads) return launch_gpt<2>(hv, sv, nblk, with_text, st);
-  if (groups <= 4 * kThreads) return launch_gpt<4>(hv, sv, nblk, with_text, st);
+  if (nvec >= kWaveVectorsMin && groups <= 4 * kWave) {
+    if (groups <= kWave) return launch_gpt<1, kWave>(hv, sv, nvec, with_text, st);
+    if (groups <= 2 * kWave) return launch_gpt<2, kWave>(hv, sv, nvec, with_text, st);
+    return launch_gpt<4, kWave>(hv, sv, nvec, with_text, st);
+  }
+  if (groups <= kThreads) return launch_gpt<1, kThreads>(hv, sv, nvec, with_text, st);
+  if (groups <= 2 * kThreads) return launch_gpt<2, kThreads>(hv, sv, nvec, with_text, st);
+  if (groups <= 4 * kThreads) return launch_gpt<4, kThreads>(hv, sv, nvec, with_text, st);
   return hipErrorInvalidValue;
 }
 

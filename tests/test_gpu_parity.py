@@ -150,6 +150,13 @@ SAMPLER = [
     (4096, 2, 4, 2.0, 0.0, 1.0, 1, 1.0),         # top-k = 1
     (512, 2, 4, 2.0, 0.0, 1.0, 0, 1e-6),         # tiny p: argmax
     (512, 2, 4, 2.0, 0.0, 1.0, 0, 0.999999),     # p near one
+    # at least 1024 vectors of at most 1024 ids: one wave per vector
+    (1024, 16, 64, 3.6, 0.0, 0.8, 20, 1.0),
+    (512, 8, 128, 2.24, 0.0, 1.0, 0, 0.95),
+    (200, 8, 128, 1.0, 0.25, 1.0, 50, 0.9),      # heavy ties at both boundaries
+    (1000, 4, 256, 0.0, 0.0, 1.0, 10, 0.5),      # all scores equal
+    (37, 32, 32, 1.0, 0.5, 1.0, 5, 0.7),
+    (256, 4, 256, 2.0, 0.0, 0.0, 0, 1.0),        # greedy
 ]
 
 
