@@ -147,14 +147,16 @@ typedef struct {
 
 /* The whole hot path of one step: projection + merge + temperature (scores),
  * text-head greedy argmax, selection, draw, pads, companion copy, grid scatter.
- * Equal to mcd_head_logits followed by mcd_sample_step: two kernel launches on
- * `stream`; no allocation, no synchronisation. */
+ * Equal to mcd_head_logits followed by mcd_sample_step: kernel launches on
+ * `stream` (a batch with both audio and text rows also runs the text
+ * projection on a second stream of the head, forked from and joined back to
+ * `stream`); no device allocation, no synchronisation. */
 mcd_status mcd_head_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
 
 /* First half of a step: the K head projections of every audio row with the
  * CFG merge (Eq. 1) and temperature applied in the GEMM epilogue, written to
  * args->scores, and the text-head projection of the TEXT rows reduced to
- * per-64-column (max, lowest argmax) partials kept in the workspace.  Tokens
+ * per-32-column (max, lowest argmax) partials kept in the workspace.  Tokens
  * and the grid are not touched. */
 mcd_status mcd_head_logits(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
 
