@@ -51,10 +51,22 @@ __device__ inline float key_to_float(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
+// Uniform loads through the constant address space, so that they become
+// scalar loads: they are counted apart from the vector loads of the scores and
+// return without waiting for them.  The buffers are read-only in this kernel.
+template <typename T>
+__device__ __forceinline__ T ld_const(const T *p, int i) {
+  return ((const __attribute__((address_space(4))) T *)p)[i];
+}
+
+// The plan header matches the step; every word is read (no short-circuit), so
+// that the loads go out together.
 __device__ inline bool plan_ok(const StepView &sv) {
   const int32_t *p = sv.plan;
-  return p[kPlanMagicWord] == kPlanMagic && p[kPlanR] == sv.R && p[kPlanPairs] == sv.n_pairs &&
-         p[kPlanSolo] == sv.n_solo && p[kPlanText] == sv.n_text;
+  const bool magic = ld_const(p, kPlanMagicWord) == kPlanMagic;
+  const bool r = ld_const(p, kPlanR) == sv.R, pairs = ld_const(p, kPlanPairs) == sv.n_pairs;
+  const bool solo = ld_const(p, kPlanSolo) == sv.n_solo, text = ld_const(p, kPlanText) == sv.n_text;
+  return magic & r & pairs & solo & text;
 }
 
 __device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
@@ -190,17 +202,16 @@ struct Smem {
     float v;
     int id;
   };
+  static constexpr int kDraw = 4 * TPV;  // every group of four ids of a vector
   uint32_t cnt[kBins + 1];               // top-k bin counts
   union {
-    unsigned long long mh[kBins + 1];    // top-p bin masses
+    unsigned long long mh[kBins + 1];    // top-p bin masses (the last: the open bin)
     unsigned long long hist[3][256];     // radix select (fallback)
-    DrawItem draw[TPV];                  // kept groups, once the selection is done
+    DrawItem draw[kDraw];                // kept groups, once the selection is done
   } u;
-  // elements of the cut bin (at most TPV), and their exact ranks
+  // elements of the cut bin (at most TPV)
   Entry le[TPV];
   unsigned long long lm[TPV];            // their masses (top-p)
-  int lr[TPV];
-  unsigned long long lsm[TPV];           // masses in rank order, then the mass before each rank
   uint32_t keepbits[TPV];                // kept cut-bin elements, one bit per slot of a thread
   uint32_t lcount;
   // reductions across the waves of a group (two slots, alternating, one barrier each)
@@ -529,23 +540,30 @@ __device__ __forceinline__ void owner_of(int e, int &thread, int &slot) {
   slot = 4 * (g / TPV) + (e & 3);
 }
 
-// Rank the listed elements of a cut bin by (score desc, id asc); n <= TPV.
-template <int TPV>
-__device__ __forceinline__ void rank_list(Smem<TPV> &sm, int n) {
+// Decide the listed elements of a cut bin (n <= TPV): entry t is ranked by
+// (score desc, id asc) against all the others; top-k keeps it when fewer than
+// `need` entries are ahead of it, top-p (MASS) when the mass ahead of it plus
+// `above` is still below `target`.  Kept entries set their owner's bit.
+template <int TPV, bool MASS>
+__device__ __forceinline__ void rank_and_keep(Smem<TPV> &sm, int n, uint64_t need,
+                                              uint64_t above, uint64_t target) {
   using Entry = typename Smem<TPV>::Entry;
   const int t = Grp<TPV>::tid();
-  if (t < n) {
-    const Entry me = sm.le[t];
-    auto ahead = [&](const Entry &o) __attribute__((always_inline)) {
-      return (int)((o.v > me.v) | ((o.v == me.v) & (o.id < me.id)));
-    };
-    int r = 0, j = 0;
-    for (; j + 4 <= n; j += 4) {
-      const Entry o0 = sm.le[j], o1 = sm.le[j + 1], o2 = sm.le[j + 2], o3 = sm.le[j + 3];
-      r += ahead(o0) + ahead(o1) + ahead(o2) + ahead(o3);
-    }
-    for (; j < n; ++j) r += ahead(sm.le[j]);
-    sm.lr[t] = r;
+  if (t >= n) return;
+  const Entry me = sm.le[t];
+  int r = 0;
+  uint64_t before = 0;
+  for (int j = 0; j < n; ++j) {
+    const Entry o = sm.le[j];
+    const bool ahead = (o.v > me.v) | ((o.v == me.v) & (o.id < me.id));
+    r += ahead ? 1 : 0;
+    if constexpr (MASS) before += ahead ? sm.lm[j] : 0ull;
+  }
+  const bool keep = MASS ? (above + before < target) : ((uint64_t)r < need);
+  if (keep) {
+    int ow, sl;
+    owner_of<TPV>(me.id, ow, sl);
+    atomicOr(&sm.keepbits[ow], 1u << sl);
   }
 }
 
@@ -591,7 +609,7 @@ __device__ __forceinline__ uint32_t radix_topp(const float (&x)[4 * GPT], uint32
 template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint32_t active,
                                                 float mx, int top_k, Smem<TPV> &sm, int &slot,
-                                                int &pass, int V) {
+                                                int &pass, int V, bool &u_dirty) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
   int bin[EPL];
@@ -610,7 +628,10 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
       if (bin[i] >= 0 && bin[i] <= bc) keep |= 1u << i;
     return keep;
   }
-  if (bc == kBins || inbin > (uint64_t)TPV) return radix_topk<GPT, TPV>(x, active, top_k, sm, slot, pass);
+  if (bc == kBins || inbin > (uint64_t)TPV) {
+    u_dirty = true;
+    return radix_topk<GPT, TPV>(x, active, top_k, sm, slot, pass);
+  }
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     if (bin[i] == bc) {
@@ -619,12 +640,7 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
     }
   }
   Grp<TPV>::sync();
-  rank_list(sm, (int)inbin);
-  if (gt < (int)inbin && (uint64_t)sm.lr[gt] < need) {
-    int ow, sl;
-    owner_of<TPV>(sm.le[gt].id, ow, sl);
-    atomicOr(&sm.keepbits[ow], 1u << sl);
-  }
+  rank_and_keep<TPV, false>(sm, (int)inbin, need, 0, 0);
   Grp<TPV>::sync();
   keep = sm.keepbits[gt];
   sm.keepbits[gt] = 0;          // next use follows at least one group barrier
@@ -635,40 +651,62 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
   return keep;
 }
 
-// top-p over the active set (the survivors of top-k); `mx` is their maximum
+// top-p over the active set (the survivors of top-k); `mx` is their maximum.
+// The mass histogram is zero on entry unless `u_dirty` (top-k used the radix
+// buffers that share its storage).
 template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint32_t active,
                                                 float mx, float top_p, Smem<TPV> &sm, int &slot,
-                                                int &pass) {
+                                                int &pass, bool u_dirty) {
   constexpr int EPL = 4 * GPT;
-  const int gt = Grp<TPV>::tid();
-  // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
-  // converted exactly to a 64-bit integer
-  uint64_t mass[EPL];
-  uint64_t zl = 0;
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
-    zl += mass[i];
+  const int gt = Grp<TPV>::tid(), lane = lane_id();
+  if (u_dirty) {   // group-uniform
+    Grp<TPV>::sync();
+    for (int b = gt; b <= kBins; b += TPV) sm.u.mh[b] = 0;
+    Grp<TPV>::sync();
   }
-  // the mass histogram shares its storage with the radix buffers, which top-k
-  // may have used: clear it once their last readers are past
-  Grp<TPV>::sync();
-  for (int b = gt; b <= kBins; b += TPV) sm.u.mh[b] = 0;
-  const uint64_t Z = grp_sum_u64<TPV>(zl, sm, slot);
-  uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
-  if (target < 1) target = 1;
-  if (target > Z) return active;
+  // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
+  // converted exactly to a 64-bit integer; every active element adds its
+  // mass to its bin (the open bin included), so the bins also give the total
+  uint64_t mass[EPL];
   int bin[EPL];
   bins_of<GPT>(x, active, mx, bin);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
   if constexpr (TPV == kWave) Grp<TPV>::sync();   // the clearing stores before the adds
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if (bin[i] >= 0 && bin[i] < kBins) atomicAdd(&sm.u.mh[bin[i]], (unsigned long long)mass[i]);
+    if (bin[i] >= 0) atomicAdd(&sm.u.mh[bin[i]], (unsigned long long)mass[i]);
   Grp<TPV>::sync();
-  uint64_t above, inbin;
-  const int bc = find_cut_bin(sm.u.mh, target, above, inbin, Z);
-  if (bc == kBins) return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
+  // every wave scans the bins: the total Z, the target ceil(p Z), the cut bin
+  uint64_t v[8], lsum = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[j] = sm.u.mh[8 * lane + j];
+    lsum += v[j];
+  }
+  const uint64_t incl = wave_incl_add_u64(lsum);
+  const uint64_t excl = incl - lsum;
+  const uint64_t Z = readlane_u64(incl, 63) + sm.u.mh[kBins];
+  uint64_t target = (uint64_t)ceil((double)top_p * (double)Z);
+  if (target < 1) target = 1;
+  if (target > Z) return active;
+  const uint64_t bal = __ballot(excl < target && incl >= target);
+  if (bal == 0) return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
+  const int src = __ffsll((long long)bal) - 1;
+  uint64_t cum = readlane_u64(excl, src), above = cum;
+  int bc = 0;
+  bool found = false;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint64_t vj = readlane_u64(v[j], src);
+    if (!found && cum + vj >= target) {
+      bc = 8 * src + j;
+      above = cum;
+      found = true;
+    }
+    cum += vj;
+  }
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     if (bin[i] == bc) {
@@ -686,22 +724,7 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
     if (gt == 0) sm.lcount = 0;
     return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
   }
-  rank_list(sm, n);
-  Grp<TPV>::sync();
-  if (gt < n) sm.lsm[sm.lr[gt]] = sm.lm[gt];
-  Grp<TPV>::sync();
-  // mass of the ranks before each rank: a group scan (thread r holds rank r)
-  const uint64_t mr = gt < n ? sm.lsm[gt] : 0;
-  const uint64_t incl = grp_incl_scan_u64<TPV>(mr, sm, slot);
-  if constexpr (TPV == kWave) Grp<TPV>::sync();   // every read of lsm before the writes
-  if (gt < n) sm.lsm[gt] = incl - mr;
-  Grp<TPV>::sync();
-  // entry kept iff the mass strictly before it (in rank order) is below target
-  if (gt < n && above + sm.lsm[sm.lr[gt]] < target) {
-    int ow, sl;
-    owner_of<TPV>(sm.le[gt].id, ow, sl);
-    atomicOr(&sm.keepbits[ow], 1u << sl);
-  }
+  rank_and_keep<TPV, true>(sm, n, 0, above, target);
   Grp<TPV>::sync();
   uint32_t keep = sm.keepbits[gt];
   sm.keepbits[gt] = 0;
@@ -715,8 +738,9 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
 template <int GPT, int TPV>
 __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
                                                uint32_t active, int V, bool greedy, int top_k,
-                                               float top_p, uint64_t rkey, int t, int k,
-                                               Smem<TPV> &sm, int &slot) {
+                                               float top_p, uint64_t rkey, int t, int k, bool pre,
+                                               const float (&gn)[4 * GPT], Smem<TPV> &sm,
+                                               int &slot) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
   uint32_t mk = 0;
@@ -741,51 +765,50 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
   }
   const float mx = key_to_float(mk);
   int pass = 0;
+  bool u_dirty = false;
   uint32_t kept = active;
-  if (top_k > 0 && top_k < V) kept = select_topk<GPT, TPV>(x, kept, mx, top_k, sm, slot, pass, V);
-  if (top_p < 1.0f) kept = select_topp<GPT, TPV>(x, kept, mx, top_p, sm, slot, pass);
+  if (top_k > 0 && top_k < V)
+    kept = select_topk<GPT, TPV>(x, kept, mx, top_k, sm, slot, pass, V, u_dirty);
+  if (top_p < 1.0f) kept = select_topp<GPT, TPV>(x, kept, mx, top_p, sm, slot, pass, u_dirty);
   // Gumbel-max over the kept ids, one Philox block per group of four ids
   double bv = -INFINITY;
   int bi = INT32_MAX;
-  if (top_k > 0 && top_k <= TPV) {
-    // few kept groups: move them to one thread each, so that no wave runs
-    // several Philox blocks one after another
-    uint32_t n = 0;
+  auto draw = [&](int g, uint32_t bits, float x0, float x1, float x2, float x3)
+                  __attribute__((always_inline)) {
+    const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
+    const float xs[4] = {x0, x1, x2, x3};
 #pragma unroll
-    for (int q = 0; q < GPT; ++q) n += ((kept >> (4 * q)) & 0xFu) ? 1u : 0u;
-    uint32_t total;
-    uint32_t pos = grp_excl_scan_u32<TPV>(n, total, sm, slot);
-    // the draw list shares its storage with the top-p histogram and the radix
-    // buffers: wait for their last readers
-    if constexpr (TPV == kWave) Grp<TPV>::sync();
-    DrawItem *dl = sm.u.draw;
+    for (int j = 0; j < 4; ++j)
+      if ((bits >> j) & 1) keep_better(bv, bi, (double)xs[j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
+  };
+  if (pre) {
+    // the noise of every id is drawn already (top-k off: a group-uniform choice)
 #pragma unroll
-    for (int q = 0; q < GPT; ++q) {
-      const uint32_t bits = (kept >> (4 * q)) & 0xFu;
-      if (bits) dl[pos++] = {q * TPV + gt, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
-    }
-    Grp<TPV>::sync();
-    if (gt < (int)total) {
-      const DrawItem it = dl[gt];
-      const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)it.g);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if ((it.bits >> j) & 1)
-          keep_better(bv, bi, (double)it.x[j] + (double)gumbel_from_word(w.w[j]), 4 * it.g + j);
-    }
+    for (int i = 0; i < EPL; ++i)
+      if ((kept >> i) & 1) keep_better(bv, bi, (double)x[i] + (double)gn[i], id_of<TPV>(i, gt));
     return grp_argmax_f64<TPV>(bv, bi, sm, slot);
   }
+  // The groups with kept ids move to an LDS list and are dealt to the threads
+  // in turn, so that the threads run the same number of Philox blocks, up to one.
+  static_assert(GPT * TPV <= Smem<TPV>::kDraw, "the draw list holds every group");
+  uint32_t n = 0;
+#pragma unroll
+  for (int q = 0; q < GPT; ++q) n += ((kept >> (4 * q)) & 0xFu) ? 1u : 0u;
+  uint32_t total;
+  uint32_t pos = grp_excl_scan_u32<TPV>(n, total, sm, slot);
+  // the list shares its storage with the histograms and radix buffers: their
+  // last readers are past the scan (or, in one wave, earlier in program order)
+  if constexpr (TPV == kWave) Grp<TPV>::sync();
+  DrawItem *dl = sm.u.draw;
 #pragma unroll
   for (int q = 0; q < GPT; ++q) {
     const uint32_t bits = (kept >> (4 * q)) & 0xFu;
-    if (bits) {
-      const int g = q * TPV + gt;
-      const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if ((bits >> j) & 1)
-          keep_better(bv, bi, (double)x[4 * q + j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
-    }
+    if (bits) dl[pos++] = {q * TPV + gt, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
+  }
+  Grp<TPV>::sync();
+  for (int e = gt; e < (int)total; e += TPV) {
+    const DrawItem it = dl[e];
+    draw(it.g, it.bits, it.x[0], it.x[1], it.x[2], it.x[3]);
   }
   return grp_argmax_f64<TPV>(bv, bi, sm, slot);
 }
@@ -799,22 +822,26 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
   __shared__ Smem<TPV> smem[G];
   Smem<TPV> &sm = smem[Grp<TPV>::index()];
   const int gt = Grp<TPV>::tid();
-  const int vec = (int)blockIdx.x * G + Grp<TPV>::index();
+  // the same for every lane of a wave: a scalar value
+  const int vec = __builtin_amdgcn_readfirstlane((int)blockIdx.x * G + Grp<TPV>::index());
   const int n_audio = sv.Rs * hv.K;
   if (vec >= n_audio + (with_text ? sv.n_text : 0)) return;   // a whole group
-  // the count histogram starts at zero (published by the first group reduction)
-  for (int b = gt; b <= kBins; b += TPV) sm.cnt[b] = 0;
+  // the histograms start at zero (published by the first group reduction)
+  for (int b = gt; b <= kBins; b += TPV) {
+    sm.cnt[b] = 0;
+    sm.u.mh[b] = 0;
+  }
   sm.keepbits[gt] = 0;
   if (gt == 0) sm.lcount = 0;
   int slot = 0;
 
-  // The scores depend only on the vector index: load them before anything
-  // else so that their latency overlaps the plan and parameter loads.
+  const bool audio = vec < n_audio;
+  const int s = audio ? vec / hv.K : 0, k = audio ? vec % hv.K : 0;
+  // The scores depend only on the vector index: their loads go out first.
   float x[EPL];
   uint32_t active = 0;
   const int V = hv.V;
-  if (vec < n_audio) {
-    const int s = vec / hv.K, k = vec % hv.K;
+  if (audio) {
     const float *sc = sv.scores + (size_t)s * hv.N + (size_t)k * V;
     if ((V & 3) == 0) {
 #pragma unroll
@@ -839,60 +866,78 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
       if (id_of<TPV>(i, gt) < V) active |= 1u << i;
   }
 
-  if (!plan_ok(sv)) {
+  // Row lookups (scalar loads): the plan rows of this vector and the row's
+  // parameters, read at a clamped index before any of them is checked, so that
+  // they are in flight together while the score loads are outstanding.
+  const bool plan_good = plan_ok(sv);
+  const int32_t *rows = sv.plan + kPlanHeader;
+  const bool paired = audio && s < sv.n_pairs;
+  const int ri = !audio ? sv.Mg + (vec - n_audio) : paired ? 2 * s : 2 * sv.n_pairs + (s - sv.n_pairs);
+  const int r = ld_const(rows, ri);
+  const int u_row = ld_const(rows, paired ? 2 * s + 1 : ri);
+  const int u = paired ? u_row : -1;
+  const bool row_ok = r >= 0 && r < sv.R && u < sv.R;
+  const int rc = row_ok ? r : 0;
+  const int t = ld_const(sv.step, rc);
+  const int nf = ld_const(sv.n_frames, rc);
+  const float T = ld_const(sv.temperature, rc), P = ld_const(sv.top_p, rc);
+  const int top_k = ld_const(sv.top_k, rc);
+  const float w_row = ld_const(sv.cfg_w, rc);
+  const float w = paired ? w_row : 0.0f;
+  const uint64_t rkey = sv.rng_key ? ld_const(sv.rng_key, rc) : (uint64_t)rc;
+  const int gslot = ld_const(sv.grid_slot, rc);
+
+  if (!plan_good) {
     if (vec == 0 && gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
     return;
   }
-  const int32_t *rows = sv.plan + kPlanHeader;
-  if (vec >= n_audio) {
+  if (!row_ok) {
+    if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    return;
+  }
+  if (!audio) {
     // text row: reduce the (max, lowest argmax) partials of the text GEMM
     const int j = vec - n_audio;
-    const int r = rows[sv.Mg + j];
-    if (r < 0 || r >= sv.R) {
-      if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-      return;
-    }
     float bv = -INFINITY;
     int bi = INT32_MAX;
     for (int p = gt; p < sv.text_parts; p += TPV)
       keep_better(bv, bi, sv.text_val[(size_t)j * sv.text_parts + p],
                   sv.text_idx[(size_t)j * sv.text_parts + p]);
     const int tok = grp_argmax_f32<TPV>(bv, bi, sm, slot);
-    for (int k = gt; k < hv.K; k += TPV)
-      sv.tokens_out[(size_t)r * hv.K + k] = (k == 0) ? tok : hv.pad_id;
+    for (int kk = gt; kk < hv.K; kk += TPV)
+      sv.tokens_out[(size_t)r * hv.K + kk] = (kk == 0) ? tok : hv.pad_id;
     return;
   }
-  const int s = vec / hv.K, k = vec % hv.K;
-  const bool paired = s < sv.n_pairs;
-  const int r = paired ? rows[2 * s] : rows[2 * sv.n_pairs + (s - sv.n_pairs)];
-  const int u = paired ? rows[2 * s + 1] : -1;
-  if (r < 0 || r >= sv.R || u >= sv.R) {
-    if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-    return;
-  }
-  const int t = sv.step[r];
   const int f = t - hv.delays.d[k];
-  const int nf = sv.n_frames[r];
   const bool pad = f < 0 || (nf >= 0 && f >= nf);
   int token = hv.pad_id;
   bool sampled = false;
   if (!pad) {
-    const float T = sv.temperature[r], P = sv.top_p[r];
-    const bool bad = !(T >= 0.0f) || isinf(T) || !(P > 0.0f) ||
-                     (paired && !isfinite(sv.cfg_w[r]));
+    const bool bad = !(T >= 0.0f) || isinf(T) || !(P > 0.0f) || (paired && !isfinite(w));
     if (bad) {
       if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
-      const uint64_t rkey = sv.rng_key ? sv.rng_key[r] : (uint64_t)r;
-      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, sv.top_k[r], P, rkey, t, k,
-                                        sm, slot);
+      // Without a top-k cut most ids stay eligible: draw the noise of every id
+      // now, while the score loads are still in flight.
+      const bool pre = T != 0.0f && !(top_k > 0 && top_k < V);
+      float gn[EPL];
+      if (pre) {
+#pragma unroll
+        for (int q = 0; q < GPT; ++q) {
+          const U64x4 wd = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k,
+                                        (uint64_t)(q * TPV + gt));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) gn[4 * q + j] = gumbel_from_word(wd.w[j]);
+        }
+      }
+      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, rkey, t, k,
+                                        pre, gn, sm, slot);
       sampled = true;
     }
   }
   if (gt == 0) {
     sv.tokens_out[(size_t)r * hv.K + k] = token;
     if (u >= 0) sv.tokens_out[(size_t)u * hv.K + k] = token;
-    const int gslot = sv.grid_slot[r];
     if (sampled && gslot >= 0 && sv.frame_grid) {
       if (gslot < sv.n_slots && f < sv.F_max)
         sv.frame_grid[((size_t)gslot * hv.K + k) * sv.F_max + f] = token;
