@@ -198,9 +198,13 @@ struct DrawItem {
 
 template <int TPV>
 struct Smem {
-  struct Entry {
+  // a cut-bin element; unused slots hold a sentinel that is never ahead of
+  // a listed element (score -inf, id INT32_MAX), so the ranking can read the
+  // list in whole blocks of kRankUnroll
+  struct alignas(16) Entry {   // read as one uint4 by the ranking
     float v;
     int id;
+    unsigned long long m;                // mass (top-p)
   };
   static constexpr int kDraw = 4 * TPV;  // every group of four ids of a vector
   uint32_t cnt[kBins + 1];               // top-k bin counts
@@ -211,7 +215,6 @@ struct Smem {
   } u;
   // elements of the cut bin (at most TPV)
   Entry le[TPV];
-  unsigned long long lm[TPV];            // their masses (top-p)
   uint32_t keepbits[TPV];                // kept cut-bin elements, one bit per slot of a thread
   uint32_t lcount;
   // reductions across the waves of a group (two slots, alternating, one barrier each)
@@ -366,6 +369,13 @@ __device__ inline float gumbel_from_word(uint64_t x) {
   return -logf(-logf(u));
 }
 
+// Top-p mass of a score: exp(s - max) in fp32 (relative error ~1e-7), scaled
+// by 2^48 and converted exactly to a 64-bit integer.  Recomputed where needed
+// (the same value every time) rather than kept in registers.
+__device__ __forceinline__ uint64_t mass_of(float s, float mx) {
+  return (uint64_t)ldexpf(expf(s - mx), 48);
+}
+
 // ---- radix select (fallback) -----------------------------------------------
 // Cut of "take `target` units from the top" among the active elements (units:
 // 1 per element, or its fixed-point mass).  Result: keep every active element
@@ -383,8 +393,8 @@ struct Cut {
 // entry, and the two after the last one used are zero again on exit.
 template <int GPT, int TPV, bool MASS>
 __device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t active,
-                                            const uint64_t *mass, uint64_t target,
-                                            Smem<TPV> &sm, int &pass) {
+                                            float mx, uint64_t target, Smem<TPV> &sm,
+                                            int &pass) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid(), lane = lane_id();
   uint32_t prefix = 0, pmask = 0;
@@ -396,7 +406,7 @@ __device__ __forceinline__ Cut radix_select(const float (&x)[4 * GPT], uint32_t 
       const uint32_t key = order_key(x[i]);
       if (((active >> i) & 1) && (key & pmask) == prefix) {
         const uint32_t d = (key >> shift) & 255u;
-        atomicAdd(&h[d], MASS ? (unsigned long long)mass[i] : 1ull);
+        atomicAdd(&h[d], MASS ? (unsigned long long)mass_of(x[i], mx) : 1ull);
       }
     }
     Grp<TPV>::sync();
@@ -540,24 +550,47 @@ __device__ __forceinline__ void owner_of(int e, int &thread, int &slot) {
   slot = 4 * (g / TPV) + (e & 3);
 }
 
+constexpr int kRankUnroll = 4;
+
+template <int TPV>
+__device__ __forceinline__ void set_sentinel(typename Smem<TPV>::Entry &e) {
+  e = {-INFINITY, INT32_MAX, 0ull};
+}
+
 // Decide the listed elements of a cut bin (n <= TPV): entry t is ranked by
 // (score desc, id asc) against all the others; top-k keeps it when fewer than
 // `need` entries are ahead of it, top-p (MASS) when the mass ahead of it plus
-// `above` is still below `target`.  Kept entries set their owner's bit.
+// `above` is still below `target`.  Kept entries set their owner's bit.  The
+// list is read in blocks of kRankUnroll (sentinels pad the last one), so that
+// the reads of a block are in flight together.
 template <int TPV, bool MASS>
 __device__ __forceinline__ void rank_and_keep(Smem<TPV> &sm, int n, uint64_t need,
                                               uint64_t above, uint64_t target) {
+  static_assert(TPV % kRankUnroll == 0, "whole blocks");
   using Entry = typename Smem<TPV>::Entry;
   const int t = Grp<TPV>::tid();
   if (t >= n) return;
   const Entry me = sm.le[t];
   int r = 0;
   uint64_t before = 0;
-  for (int j = 0; j < n; ++j) {
-    const Entry o = sm.le[j];
-    const bool ahead = (o.v > me.v) | ((o.v == me.v) & (o.id < me.id));
-    r += ahead ? 1 : 0;
-    if constexpr (MASS) before += ahead ? sm.lm[j] : 0ull;
+  for (int j = 0; j < n; j += kRankUnroll) {
+    uint4 o[kRankUnroll];   // whole 16-byte entries: v, id, m (low, high)
+#pragma unroll
+    for (int q = 0; q < kRankUnroll; ++q) o[q] = *reinterpret_cast<const uint4 *>(&sm.le[j + q]);
+#pragma unroll
+    for (int q = 0; q < kRankUnroll; ++q) {
+      const float ov = __uint_as_float(o[q].x);
+      const int oid = (int)o[q].y;
+      const bool ahead = (ov > me.v) | ((ov == me.v) & (oid < me.id));
+      r += ahead ? 1 : 0;
+      if constexpr (MASS) {
+        // an opaque mask rather than a select: the mass read then stays in
+        // the batch instead of becoming a read behind a branch
+        uint32_t msk = ahead ? 0xFFFFFFFFu : 0u;
+        asm volatile("" : "+v"(msk));
+        before += (uint64_t)(o[q].w & msk) << 32 | (o[q].z & msk);
+      }
+    }
   }
   const bool keep = MASS ? (above + before < target) : ((uint64_t)r < need);
   if (keep) {
@@ -565,6 +598,36 @@ __device__ __forceinline__ void rank_and_keep(Smem<TPV> &sm, int n, uint64_t nee
     owner_of<TPV>(me.id, ow, sl);
     atomicOr(&sm.keepbits[ow], 1u << sl);
   }
+}
+
+// Append the active elements of bin `bc` to the cut-bin list: one list
+// reservation per thread.  Slots at or beyond TPV are not written (the caller
+// falls back to the radix select when the count exceeds TPV).
+template <int GPT, int TPV, bool MASS>
+__device__ __forceinline__ void list_bin(Smem<TPV> &sm, const float (&x)[4 * GPT],
+                                         const int (&bin)[4 * GPT], int bc, float mx) {
+  constexpr int EPL = 4 * GPT;
+  const int gt = Grp<TPV>::tid();
+  uint32_t c = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) c += bin[i] == bc ? 1u : 0u;
+  if (c == 0) return;
+  uint32_t pos = atomicAdd(&sm.lcount, c);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    if (bin[i] == bc) {
+      if (pos < (uint32_t)TPV) sm.le[pos] = {x[i], id_of<TPV>(i, gt), MASS ? mass_of(x[i], mx) : 0ull};
+      ++pos;
+    }
+  }
+}
+
+// After a ranking: the list slots go back to the sentinel (the next list
+// build follows at least one group barrier).
+template <int TPV>
+__device__ __forceinline__ void clear_list(Smem<TPV> &sm, int n) {
+  const int t = Grp<TPV>::tid();
+  if (t < n) set_sentinel<TPV>(sm.le[t]);
 }
 
 // The radix buffers alias the top-p histogram: wait for its last readers.
@@ -579,23 +642,23 @@ template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t radix_topk(const float (&x)[4 * GPT], uint32_t active,
                                                int top_k, Smem<TPV> &sm, int &slot, int &pass) {
   zero_radix(sm);
-  const Cut c = radix_select<GPT, TPV, false>(x, active, nullptr, (uint64_t)top_k, sm, pass);
+  const Cut c = radix_select<GPT, TPV, false>(x, active, 0.0f, (uint64_t)top_k, sm, pass);
   return apply_cut<GPT, TPV>(x, active, c, c.need, sm, slot);
 }
 
 template <int GPT, int TPV>
 __device__ __forceinline__ uint32_t radix_topp(const float (&x)[4 * GPT], uint32_t active,
-                                               const uint64_t (&mass)[4 * GPT], uint64_t target,
-                                               Smem<TPV> &sm, int &slot, int &pass) {
+                                               float mx, uint64_t target, Smem<TPV> &sm,
+                                               int &slot, int &pass) {
   zero_radix(sm);
-  const Cut c = radix_select<GPT, TPV, true>(x, active, mass, target, sm, pass);
+  const Cut c = radix_select<GPT, TPV, true>(x, active, mx, target, sm, pass);
   uint64_t need_n = 0;
   if (c.exact) {
     // every element tied at kappa carries the same mass q: the fewest reaching rem
     uint64_t q = 0;
 #pragma unroll
     for (int i = 0; i < 4 * GPT; ++i)
-      if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass[i];
+      if (((active >> i) & 1) && order_key(x[i]) == c.lo) q = mass_of(x[i], mx);
     // every nonzero q is the same value, so the halves reduce independently
     const uint64_t qhi = grp_max_u32<TPV>((uint32_t)(q >> 32), sm, slot);
     const uint64_t qlo = grp_max_u32<TPV>((uint32_t)q, sm, slot);
@@ -632,16 +695,11 @@ __device__ __forceinline__ uint32_t select_topk(const float (&x)[4 * GPT], uint3
     u_dirty = true;
     return radix_topk<GPT, TPV>(x, active, top_k, sm, slot, pass);
   }
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    if (bin[i] == bc) {
-      const int s = (int)atomicAdd(&sm.lcount, 1u);
-      sm.le[s] = {x[i], id_of<TPV>(i, gt)};
-    }
-  }
+  list_bin<GPT, TPV, false>(sm, x, bin, bc, 0.0f);
   Grp<TPV>::sync();
   rank_and_keep<TPV, false>(sm, (int)inbin, need, 0, 0);
   Grp<TPV>::sync();
+  clear_list<TPV>(sm, (int)inbin);
   keep = sm.keepbits[gt];
   sm.keepbits[gt] = 0;          // next use follows at least one group barrier
   if (gt == 0) sm.lcount = 0;
@@ -665,18 +723,14 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
     for (int b = gt; b <= kBins; b += TPV) sm.u.mh[b] = 0;
     Grp<TPV>::sync();
   }
-  // mass = exp(s - max) in fp32 (relative error ~1e-7), scaled by 2^48 and
-  // converted exactly to a 64-bit integer; every active element adds its
-  // mass to its bin (the open bin included), so the bins also give the total
-  uint64_t mass[EPL];
+  // every active element adds its mass to its bin (the open bin included), so
+  // the bins also give the total
   int bin[EPL];
   bins_of<GPT>(x, active, mx, bin);
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) mass[i] = ((active >> i) & 1) ? (uint64_t)ldexpf(expf(x[i] - mx), 48) : 0;
   if constexpr (TPV == kWave) Grp<TPV>::sync();   // the clearing stores before the adds
 #pragma unroll
   for (int i = 0; i < EPL; ++i)
-    if (bin[i] >= 0) atomicAdd(&sm.u.mh[bin[i]], (unsigned long long)mass[i]);
+    if (bin[i] >= 0) atomicAdd(&sm.u.mh[bin[i]], (unsigned long long)mass_of(x[i], mx));
   Grp<TPV>::sync();
   // every wave scans the bins: the total Z, the target ceil(p Z), the cut bin
   uint64_t v[8], lsum = 0;
@@ -692,7 +746,7 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
   if (target < 1) target = 1;
   if (target > Z) return active;
   const uint64_t bal = __ballot(excl < target && incl >= target);
-  if (bal == 0) return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
+  if (bal == 0) return radix_topp<GPT, TPV>(x, active, mx, target, sm, slot, pass);
   const int src = __ffsll((long long)bal) - 1;
   uint64_t cum = readlane_u64(excl, src), above = cum;
   int bc = 0;
@@ -707,25 +761,18 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
     }
     cum += vj;
   }
-#pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    if (bin[i] == bc) {
-      const int s = (int)atomicAdd(&sm.lcount, 1u);
-      if (s < TPV) {
-        sm.le[s] = {x[i], id_of<TPV>(i, gt)};
-        sm.lm[s] = mass[i];
-      }
-    }
-  }
+  list_bin<GPT, TPV, true>(sm, x, bin, bc, mx);
   Grp<TPV>::sync();
   const int n = (int)sm.lcount;
   if (n > TPV) {
     Grp<TPV>::sync();   // everyone has read lcount
     if (gt == 0) sm.lcount = 0;
-    return radix_topp<GPT, TPV>(x, active, mass, target, sm, slot, pass);
+    clear_list<TPV>(sm, TPV);
+    return radix_topp<GPT, TPV>(x, active, mx, target, sm, slot, pass);
   }
   rank_and_keep<TPV, true>(sm, n, 0, above, target);
   Grp<TPV>::sync();
+  clear_list<TPV>(sm, n);
   uint32_t keep = sm.keepbits[gt];
   sm.keepbits[gt] = 0;
   if (gt == 0) sm.lcount = 0;
@@ -832,6 +879,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     sm.u.mh[b] = 0;
   }
   sm.keepbits[gt] = 0;
+  set_sentinel<TPV>(sm.le[gt]);
   if (gt == 0) sm.lcount = 0;
   int slot = 0;
 
