@@ -340,6 +340,18 @@ struct U64x4 {
   uint64_t w[4];
 };
 
+// Full 64 x 64 -> 128-bit product from four 32 x 32 -> 64-bit partial
+// products, each a multiply-add whose addend cannot overflow it.
+__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t b, uint64_t &lo, uint64_t &hi) {
+  const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+  const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+  const uint64_t p00 = (uint64_t)a0 * b0;
+  const uint64_t p01 = (uint64_t)a0 * b1 + (p00 >> 32);
+  const uint64_t p10 = (uint64_t)a1 * b0 + (uint32_t)p01;
+  hi = (uint64_t)a1 * b1 + ((p01 >> 32) + (p10 >> 32));
+  lo = (p10 << 32) | (uint32_t)p00;
+}
+
 __device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, uint64_t k,
                                      uint64_t group) {
   const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
@@ -351,8 +363,9 @@ __device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, ui
       k0 += 0x9E3779B97F4A7C15ull;
       k1 += 0xBB67AE8584CAA73Bull;
     }
-    const uint64_t lo0 = m0 * x0, hi0 = __umul64hi(m0, x0);
-    const uint64_t lo1 = m1 * x2, hi1 = __umul64hi(m1, x2);
+    uint64_t lo0, hi0, lo1, hi1;
+    mulhilo64(m0, x0, lo0, hi0);
+    mulhilo64(m1, x2, lo1, hi1);
     const uint64_t y0 = hi1 ^ x1 ^ k0, y2 = hi0 ^ x3 ^ k1;
     x0 = y0;
     x1 = lo1;
@@ -362,11 +375,14 @@ __device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, ui
   return U64x4{{x0, x1, x2, x3}};
 }
 
-// Gumbel variate from one Philox word, in fp32 (the uniform is exact in fp32;
-// each log is within about one ulp, so G is within ~1e-6 of its exact value).
+// Gumbel variate from one Philox word, in fp32.  The uniform is exact in fp32;
+// with base-2 logarithms, -ln(-ln u) = -ln(ln 2) - ln 2 * log2(-log2 u), and
+// both log2 inputs are normal numbers (-log2 u >= 2^-24 / ln 2), where the
+// hardware log2 is accurate to about one ulp: G is within ~1e-6 of its value.
 __device__ inline float gumbel_from_word(uint64_t x) {
   const float u = ((float)(uint32_t)(x >> 41) + 0.5f) * 0x1p-23f;
-  return -logf(-logf(u));
+  const float e = -__builtin_amdgcn_logf(u);   // -log2 u, in (0, 23]
+  return fmaf(-0.69314718055994531f, __builtin_amdgcn_logf(e), 0.36651292058166435f);
 }
 
 // Top-p mass of a score: exp(s - max) in fp32 (relative error ~1e-7), scaled
