@@ -51,6 +51,9 @@ def lib():
         u64p = ctypes.POINTER(ctypes.c_uint64)
         L.orc_philox4x64_10.argtypes = [u64p, u64p, u64p]
         L.orc_philox4x64_10.restype = None
+        u32p = ctypes.POINTER(ctypes.c_uint32)
+        L.orc_philox4x32_10.argtypes = [u32p, u32p, u32p]
+        L.orc_philox4x32_10.restype = None
         L.orc_uniform.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64,
                                   ctypes.c_int32, ctypes.c_int32]
         L.orc_uniform.restype = ctypes.c_double
@@ -120,6 +123,17 @@ def philox4x64_10(ctr, key):
     u64p = ctypes.POINTER(ctypes.c_uint64)
     lib().orc_philox4x64_10(c.ctypes.data_as(u64p), k.ctypes.data_as(u64p),
                             out.ctypes.data_as(u64p))
+    return out
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32-10 block: four 32-bit counter words, two key words -> four words."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    lib().orc_philox4x32_10(c.ctypes.data_as(u32p), k.ctypes.data_as(u32p),
+                            out.ctypes.data_as(u32p))
     return out
 
 

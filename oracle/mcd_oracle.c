@@ -44,16 +44,44 @@ void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t ou
   out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
 }
 
-/* Counter layout: (v / 4, k, t, rng_key), key (seed, 0), word v mod 4.  The
- * top 23 bits of the word, plus one half, scaled by 2^-23: a uniform on the
- * open interval (0,1) that is exact in fp32 and fp64. */
+/* Philox4x32-10, from the same paper: ten rounds of the 4x32 S-box (two
+ * 32x32->64 multiplies, hi/lo words xor-ed with the other counter words and the
+ * round key), with the key bumped by the two 32-bit Weyl constants between
+ * rounds; multiplier and Weyl constants as published there. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) { k0 += W0; k1 += W1; }
+    uint64_t p0 = (uint64_t)M0 * x0;
+    uint64_t p1 = (uint64_t)M1 * x2;
+    uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    uint32_t y1 = (uint32_t)p1;
+    uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    uint32_t y3 = (uint32_t)p0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* Two levels of counter-based Philox.  The key material of the vector
+ * (request rng_key, step t, codebook k): D = Philox4x64-10 at counter
+ * (0, k, t, rng_key) with key (seed, 0).  Element v: word v mod 4 of
+ * Philox4x32-10 at counter (v / 4, lo D1, hi D1, lo D2) with key (lo D0, hi D0).
+ * Its top 23 bits, plus one half, scaled by 2^-23: a uniform on the open
+ * interval (0,1) that is exact in fp32 and fp64. */
 double orc_uniform(uint64_t seed, uint64_t rng_key, int64_t t, int32_t k, int32_t v) {
-  uint64_t ctr[4] = {(uint64_t)(v >> 2), (uint64_t)k, (uint64_t)t, rng_key};
-  uint64_t key[2] = {seed, 0};
-  uint64_t w[4];
-  orc_philox4x64_10(ctr, key, w);
-  uint64_t x = w[v & 3];
-  return ((double)(x >> 41) + 0.5) * ldexp(1.0, -23);
+  uint64_t c64[4] = {0, (uint64_t)k, (uint64_t)t, rng_key};
+  uint64_t k64[2] = {seed, 0};
+  uint64_t d[4];
+  orc_philox4x64_10(c64, k64, d);
+  uint32_t c32[4] = {(uint32_t)(v >> 2), (uint32_t)d[1], (uint32_t)(d[1] >> 32), (uint32_t)d[2]};
+  uint32_t k32[2] = {(uint32_t)d[0], (uint32_t)(d[0] >> 32)};
+  uint32_t w[4];
+  orc_philox4x32_10(c32, k32, w);
+  return ((double)(w[v & 3] >> 9) + 0.5) * ldexp(1.0, -23);
 }
 
 /* Gumbel(0,1) by inversion of its CDF exp(-exp(-g)). */

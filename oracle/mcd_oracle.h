@@ -76,6 +76,9 @@ typedef struct {
 /* Philox4x64 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11). */
 void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
 
+/* Philox4x32 with 10 rounds (same paper). */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
 /* Uniform in (0,1) for element v of codebook k of request rng_key at step t. */
 double orc_uniform(uint64_t seed, uint64_t rng_key, int64_t t, int32_t k, int32_t v);
 

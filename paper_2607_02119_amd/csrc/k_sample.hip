@@ -9,14 +9,17 @@
 //   * top-p: over the survivors, keep the shortest (score desc, id asc) prefix
 //     whose softmax mass reaches p;
 //   * Gumbel-max: token = argmax over kept ids of s_v + G_v, G_v = -log(-log u_v),
-//     u_v from Philox4x64-10 with counter (v/4, k, t, rng_key), key (seed, 0),
-//     word v mod 4, u = (top 23 bits + 1/2) * 2^-23; lowest id on ties;
+//     lowest id on ties.  Counter-based Philox (Salmon, Moraes, Dror, Shaw,
+//     SC'11) in two levels: the vector's key material D = Philox4x64-10 with
+//     counter (0, k, t, rng_key) and key (seed, 0), once per vector; then for
+//     id v the word v mod 4 of Philox4x32-10 with counter (v/4, lo D1, hi D1,
+//     lo D2) and key (lo D0, hi D0); u = (top 23 bits + 1/2) * 2^-23;
 //   * the token goes to the Main row, to its Companion (Sec. 2.4) and to the
 //     request's frame grid cell [k][f].
 //
 // Layout: thread tid owns groups g = q * 256 + tid of four consecutive ids
-// 4g .. 4g + 3 (one 16-byte load each), so that one Philox block serves a whole
-// group from registers.
+// 4g .. 4g + 3 (one 16-byte load each), so that one Philox4x32 block serves a
+// whole group from registers.
 //
 // Selection.  Every score s falls in a bin b = floor(16 (max - s)) (bins of
 // width 1/16 below the maximum, the last one open-ended); the bin index is
@@ -217,11 +220,13 @@ struct Smem {
   Entry le[TPV];
   uint32_t keepbits[TPV];                // kept cut-bin elements, one bit per slot of a thread
   uint32_t lcount;
+  uint32_t nkw[5];                       // the vector's noise key, from its first wave
   // reductions across the waves of a group (two slots, alternating, one barrier each)
   uint32_t ru[2][Grp<TPV>::kGW];
   unsigned long long r64[2][Grp<TPV>::kGW];
   double rd[2][Grp<TPV>::kGW];
   int ri[2][Grp<TPV>::kGW];
+  float rx[2][Grp<TPV>::kGW];
 };
 
 template <int TPV>
@@ -335,7 +340,60 @@ __device__ __forceinline__ int grp_argmax_f64(double bv, int bi, Smem<TPV> &sm, 
   return ri;
 }
 
-// ---- Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11) ---------------------
+// A draw candidate: its perturbed score s = x + G (fp64, exact), its id and
+// its score x.  Candidates order by (s desc, id asc).
+struct Cand {
+  double s;
+  int id;
+  float x;
+};
+
+__device__ __forceinline__ void keep_cand(Cand &b, double s, int id, float x) {
+  if (s > b.s || (s == b.s && id < b.id)) b = {s, id, x};
+}
+
+// One group reduction of both a 64-bit sum and the best candidate (a single
+// barrier for a workgroup group); every thread gets both.
+template <int TPV>
+__device__ __forceinline__ Cand grp_sum_and_best(uint64_t &sum, Cand c, Smem<TPV> &sm, int &slot) {
+  const uint64_t ninf = (uint64_t)__double_as_longlong(-INFINITY);
+  wave_scan([&](auto cc, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(cc)::value, RM = decltype(m)::value;
+    const uint32_t slo = dpp<C, RM>(0u, (uint32_t)sum), shi = dpp<C, RM>(0u, (uint32_t)(sum >> 32));
+    const uint64_t b = (uint64_t)__double_as_longlong(c.s);
+    const uint32_t lo = dpp<C, RM>((uint32_t)ninf, (uint32_t)b);
+    const uint32_t hi = dpp<C, RM>((uint32_t)(ninf >> 32), (uint32_t)(b >> 32));
+    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)c.id);
+    const float ox = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.x)));
+    sum += ((uint64_t)shi << 32) | slo;
+    keep_cand(c, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oi, ox);
+  });
+  sum = readlane_u64(sum, 63);
+  c.s = __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(c.s), 63));
+  c.id = __builtin_amdgcn_readlane(c.id, 63);
+  c.x = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.x), 63));
+  if constexpr (TPV == kWave) return c;
+  if (lane_id() == 0) {
+    const int w = Grp<TPV>::wave();
+    sm.r64[slot][w] = sum;
+    sm.rd[slot][w] = c.s;
+    sm.ri[slot][w] = c.id;
+    sm.rx[slot][w] = c.x;
+  }
+  Grp<TPV>::sync();
+  uint64_t t = 0;
+  Cand r = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) {
+    t += sm.r64[slot][w];
+    keep_cand(r, sm.rd[slot][w], sm.ri[slot][w], sm.rx[slot][w]);
+  }
+  slot ^= 1;
+  sum = t;
+  return r;
+}
+
+// ---- Philox (Salmon, Moraes, Dror, Shaw, SC'11) ------------------------------
 struct U64x4 {
   uint64_t w[4];
 };
@@ -352,11 +410,11 @@ __device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t b, uint64_t &lo, 
   lo = (p10 << 32) | (uint32_t)p00;
 }
 
-__device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, uint64_t k,
-                                     uint64_t group) {
+// Philox4x64-10: counter (x0, x1, x2, x3), key (k0, 0).
+__device__ __forceinline__ U64x4 philox4x64(uint64_t x0, uint64_t x1, uint64_t x2, uint64_t x3,
+                                   uint64_t k0) {
   const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
-  uint64_t x0 = group, x1 = k, x2 = t, x3 = key;
-  uint64_t k0 = seed, k1 = 0;
+  uint64_t k1 = 0;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r) {
@@ -375,12 +433,48 @@ __device__ inline U64x4 philox_block(uint64_t seed, uint64_t key, uint64_t t, ui
   return U64x4{{x0, x1, x2, x3}};
 }
 
+// The key material of one vector: Philox4x32-10 key (k0, k1) and counter
+// words 1..3 of every id's block.
+struct NoiseKey {
+  uint32_t k0, k1, c1, c2, c3;
+};
+
+__device__ __forceinline__ NoiseKey noise_key(uint64_t seed, uint64_t rng_key, int t, int k) {
+  const U64x4 d = philox4x64(0, (uint64_t)k, (uint64_t)t, rng_key, seed);
+  return NoiseKey{(uint32_t)d.w[0], (uint32_t)(d.w[0] >> 32), (uint32_t)d.w[1],
+                  (uint32_t)(d.w[1] >> 32), (uint32_t)d.w[2]};
+}
+
+struct U32x4 {
+  uint32_t w[4];
+};
+
+// Philox4x32-10 block of the ids 4g .. 4g + 3 of a vector: counter
+// (g, c1, c2, c3), key (k0, k1); each round is two 32 x 32 -> 64-bit products.
+__device__ __forceinline__ U32x4 noise_block(const NoiseKey &nk, uint32_t g) {
+  uint32_t x0 = g, x1 = nk.c1, x2 = nk.c2, x3 = nk.c3, k0 = nk.k0, k1 = nk.k1;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * x0, p1 = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0, y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    x0 = y0;
+    x1 = (uint32_t)p1;
+    x2 = y2;
+    x3 = (uint32_t)p0;
+  }
+  return U32x4{{x0, x1, x2, x3}};
+}
+
 // Gumbel variate from one Philox word, in fp32.  The uniform is exact in fp32;
 // with base-2 logarithms, -ln(-ln u) = -ln(ln 2) - ln 2 * log2(-log2 u), and
 // both log2 inputs are normal numbers (-log2 u >= 2^-24 / ln 2), where the
 // hardware log2 is accurate to about one ulp: G is within ~1e-6 of its value.
-__device__ inline float gumbel_from_word(uint64_t x) {
-  const float u = ((float)(uint32_t)(x >> 41) + 0.5f) * 0x1p-23f;
+__device__ __forceinline__ float gumbel_from_word(uint32_t x) {
+  const float u = ((float)(x >> 9) + 0.5f) * 0x1p-23f;
   const float e = -__builtin_amdgcn_logf(u);   // -log2 u, in (0, 23]
   return fmaf(-0.69314718055994531f, __builtin_amdgcn_logf(e), 0.36651292058166435f);
 }
@@ -798,11 +892,55 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
   return keep;
 }
 
+// Draw without a top-k cut, the noise gn of every id drawn already.  The token
+// is the best candidate (s desc, id asc) inside the nucleus, and the nucleus
+// is a prefix of the score order (x desc, id asc): an element is inside iff
+// the mass strictly ahead of it is below the target ceil(p Z).  So test the
+// best candidate c; if it is outside, so is every element behind it, and the
+// next candidate is the best one ahead of c.  Each test is one group sum
+// (mass ahead of c), taken together with the next candidate (best ahead of
+// c).  The first element of the score order has nothing ahead of it, so the
+// loop ends; the sampled candidate is outside with probability 1 - p.
+template <int GPT, int TPV>
+__device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], const float (&gn)[4 * GPT],
+                                            uint32_t active, float mx, float top_p,
+                                            Smem<TPV> &sm, int &slot) {
+  constexpr int EPL = 4 * GPT;
+  const int gt = Grp<TPV>::tid();
+  uint64_t mass[EPL], z = 0;
+  Cand c = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    mass[i] = ((active >> i) & 1) ? mass_of(x[i], mx) : 0ull;
+    z += mass[i];
+    if ((active >> i) & 1) keep_cand(c, (double)x[i] + (double)gn[i], id_of<TPV>(i, gt), x[i]);
+  }
+  c = grp_sum_and_best<TPV>(z, c, sm, slot);
+  if (!(top_p < 1.0f)) return c.id;
+  uint64_t target = (uint64_t)ceil((double)top_p * (double)z);
+  if (target < 1) target = 1;
+  if (target > z) return c.id;
+  for (;;) {   // group-uniform
+    uint64_t a = 0;
+    Cand nc = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int id = id_of<TPV>(i, gt);
+      if (((active >> i) & 1) && ((x[i] > c.x) | ((x[i] == c.x) & (id < c.id)))) {
+        a += mass[i];
+        keep_cand(nc, (double)x[i] + (double)gn[i], id, x[i]);
+      }
+    }
+    nc = grp_sum_and_best<TPV>(a, nc, sm, slot);
+    if (a < target) return c.id;
+    c = nc;
+  }
+}
+
 template <int GPT, int TPV>
 __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
                                                uint32_t active, int V, bool greedy, int top_k,
-                                               float top_p, uint64_t rkey, int t, int k, bool pre,
-                                               const float (&gn)[4 * GPT], Smem<TPV> &sm,
+                                               float top_p, bool pre, Smem<TPV> &sm,
                                                int &slot) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
@@ -827,6 +965,19 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     return (int)grp_min_u32<TPV>(id, sm, slot);
   }
   const float mx = key_to_float(mk);
+  // the noise key, published by the barrier of the maximum
+  const NoiseKey nk{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
+  if (pre) {
+    // the noise of every id (the candidates are tested in perturbed-score order)
+    float gn[EPL];
+#pragma unroll
+    for (int q = 0; q < GPT; ++q) {
+      const U32x4 wd = noise_block(nk, (uint32_t)(q * TPV + gt));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gn[4 * q + j] = gumbel_from_word(wd.w[j]);
+    }
+    return draw_nucleus<GPT, TPV>(x, gn, active, mx, top_p, sm, slot);
+  }
   int pass = 0;
   bool u_dirty = false;
   uint32_t kept = active;
@@ -838,19 +989,12 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
   int bi = INT32_MAX;
   auto draw = [&](int g, uint32_t bits, float x0, float x1, float x2, float x3)
                   __attribute__((always_inline)) {
-    const U64x4 w = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k, (uint64_t)g);
+    const U32x4 w = noise_block(nk, (uint32_t)g);
     const float xs[4] = {x0, x1, x2, x3};
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       if ((bits >> j) & 1) keep_better(bv, bi, (double)xs[j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
   };
-  if (pre) {
-    // the noise of every id is drawn already (top-k off: a group-uniform choice)
-#pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if ((kept >> i) & 1) keep_better(bv, bi, (double)x[i] + (double)gn[i], id_of<TPV>(i, gt));
-    return grp_argmax_f64<TPV>(bv, bi, sm, slot);
-  }
   // The groups with kept ids move to an LDS list and are dealt to the threads
   // in turn, so that the threads run the same number of Philox blocks, up to one.
   static_assert(GPT * TPV <= Smem<TPV>::kDraw, "the draw list holds every group");
@@ -981,21 +1125,22 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     if (bad) {
       if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
-      // Without a top-k cut most ids stay eligible: draw the noise of every id
-      // now, while the score loads are still in flight.
+      // Without a top-k cut the draw tests candidates in perturbed-score order
+      // against the nucleus, which takes the noise of every id.
       const bool pre = T != 0.0f && !(top_k > 0 && top_k < V);
-      float gn[EPL];
-      if (pre) {
-#pragma unroll
-        for (int q = 0; q < GPT; ++q) {
-          const U64x4 wd = philox_block(sv.seed, rkey, (uint64_t)t, (uint64_t)k,
-                                        (uint64_t)(q * TPV + gt));
-#pragma unroll
-          for (int j = 0; j < 4; ++j) gn[4 * q + j] = gumbel_from_word(wd.w[j]);
+      // The vector's noise key: 64-bit multiplies on uniform values (scalar
+      // unit), so one wave computes it for the group.
+      if (T != 0.0f && Grp<TPV>::wave() == 0) {
+        const NoiseKey nk = noise_key(sv.seed, rkey, t, k);
+        if (lane_id() == 0) {
+          sm.nkw[0] = nk.k0;
+          sm.nkw[1] = nk.k1;
+          sm.nkw[2] = nk.c1;
+          sm.nkw[3] = nk.c2;
+          sm.nkw[4] = nk.c3;
         }
       }
-      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, rkey, t, k,
-                                        pre, gn, sm, slot);
+      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, pre, sm, slot);
       sampled = true;
     }
   }

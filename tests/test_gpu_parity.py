@@ -150,6 +150,11 @@ SAMPLER = [
     (4096, 2, 4, 2.0, 0.0, 1.0, 1, 1.0),         # top-k = 1
     (512, 2, 4, 2.0, 0.0, 1.0, 0, 1e-6),         # tiny p: argmax
     (512, 2, 4, 2.0, 0.0, 1.0, 0, 0.999999),     # p near one
+    # no top-k cut: candidates in perturbed-score order tested against the nucleus
+    (4096, 4, 4, 2.0, 0.0, 1.0, 0, 1.0),         # plain sampling
+    (4096, 4, 8, 1.0, 0.25, 1.0, 0, 0.3),        # small p, heavy ties: several candidates
+    (1000, 2, 3, 0.0, 0.0, 1.0, 0, 0.5),         # all scores equal: the nucleus is by id
+    (37, 3, 5, 1.0, 0.5, 1.0, 37, 0.7),          # top-k = V is no cut
     # at least 1024 vectors of at most 1024 ids: one wave per vector
     (1024, 16, 64, 3.6, 0.0, 0.8, 20, 1.0),
     (512, 8, 128, 2.24, 0.0, 1.0, 0, 0.95),
@@ -157,6 +162,8 @@ SAMPLER = [
     (1000, 4, 256, 0.0, 0.0, 1.0, 10, 0.5),      # all scores equal
     (37, 32, 32, 1.0, 0.5, 1.0, 5, 0.7),
     (256, 4, 256, 2.0, 0.0, 0.0, 0, 1.0),        # greedy
+    (256, 4, 256, 1.0, 0.25, 1.0, 0, 0.3),       # no top-k cut, small p, heavy ties
+    (1000, 4, 256, 0.0, 0.0, 1.0, 0, 0.5),       # no top-k cut, all scores equal
 ]
 
 

@@ -21,7 +21,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 # ----------------------------------------------------------------------------
-# Philox4x64-10 and the uniform / Gumbel draw
+# Philox4x64-10, Philox4x32-10 and the uniform / Gumbel draw
 
 def _numpy_philox(ctr, key):
     """numpy's Philox4x64-10 block at counter ctr (numpy pre-increments, so seed ctr-1)."""
@@ -42,6 +42,16 @@ def test_philox_known_answers():
         assert [int(x) for x in out] == w[6:10]
 
 
+def test_philox4x32_known_answers():
+    rows = [ln.split() for ln in open(os.path.join(GOLDEN, "philox4x32_10_kat.txt"))
+            if ln.strip() and not ln.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        w = [int(x, 16) for x in r]
+        out = oracle.philox4x32_10(w[0:4], w[4:6])
+        assert [int(x) for x in out] == w[6:10]
+
+
 def test_philox_matches_numpy_random_counters():
     rng = np.random.default_rng(123)
     for _ in range(300):
@@ -52,12 +62,26 @@ def test_philox_matches_numpy_random_counters():
 
 
 def test_uniform_uses_the_stated_counter_layout():
-    # counter (v>>2, k, t, rng_key), key (seed, 0), word v & 3, top 23 bits + 1/2
-    for (seed, key, t, k, v) in [(0, 0, 0, 0, 0), (0, 7, 13, 3, 1022), (5, 2**40 + 3, 511, 7, 4095)]:
-        w = _numpy_philox([v >> 2, k, t, key], [seed, 0])[v & 3]
+    # D = Philox4x64-10 at counter (0, k, t, rng_key), key (seed, 0) (numpy's block);
+    # element v: word v & 3 of Philox4x32-10 at counter (v >> 2, lo D1, hi D1, lo D2),
+    # key (lo D0, hi D0) (the block pinned by its known answers); top 23 bits + 1/2
+    lo = lambda x: int(x) & 0xFFFFFFFF
+    hi = lambda x: int(x) >> 32
+    for (seed, key, t, k, v) in [(0, 0, 0, 0, 0), (0, 7, 13, 3, 1022), (5, 2**40 + 3, 511, 7, 4095),
+                                 (2**63 + 9, 2**64 - 1, 2**31 - 1, 15, 151935)]:
+        d = _numpy_philox([0, k, t, key], [seed, 0])
+        w = oracle.philox4x32_10([v >> 2, lo(d[1]), hi(d[1]), lo(d[2])], [lo(d[0]), hi(d[0])])[v & 3]
         u = oracle.uniform(seed, key, t, k, v)
-        assert u == ((int(w) >> 41) + 0.5) / 2**23
+        assert u == ((int(w) >> 9) + 0.5) / 2**23
         assert 0.0 < u < 1.0
+
+
+def test_uniform_streams_differ_per_coordinate():
+    # every coordinate of the key material changes the stream
+    base = [oracle.uniform(3, 11, 40, 2, v) for v in range(64)]
+    for args in [(4, 11, 40, 2), (3, 12, 40, 2), (3, 11, 41, 2), (3, 11, 40, 3)]:
+        other = [oracle.uniform(*args, v) for v in range(64)]
+        assert sum(a == b for a, b in zip(base, other)) <= 2
 
 
 def test_uniform_is_exact_and_uniform():
