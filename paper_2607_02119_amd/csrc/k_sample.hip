@@ -8,8 +8,8 @@
 //   * top-k: keep the k largest scores, ties at the boundary to the lowest ids;
 //   * top-p: over the survivors, keep the shortest (score desc, id asc) prefix
 //     whose softmax mass reaches p;
-//   * Gumbel-max: token = argmax over kept ids of s_v + G_v, G_v = -log(-log u_v),
-//     lowest id on ties.  Counter-based Philox (Salmon, Moraes, Dror, Shaw,
+//   * Gumbel-max: token = argmax over kept ids of s_v + G_v, G_v = -log(-log u_v)
+//     (G and the sum in fp32), lowest id on ties.  Counter-based Philox (Salmon, Moraes, Dror, Shaw,
 //     SC'11) in two levels: the vector's key material D = Philox4x64-10 with
 //     counter (0, k, t, rng_key) and key (seed, 0), once per vector; then for
 //     id v the word v mod 4 of Philox4x32-10 with counter (v/4, lo D1, hi D1,
@@ -154,20 +154,6 @@ __device__ __forceinline__ void wave_argmax_f32(float &bv, int &bi) {
   bi = __builtin_amdgcn_readlane(bi, 63);
 }
 
-__device__ __forceinline__ void wave_argmax_f64(double &bv, int &bi) {
-  const uint64_t ninf = (uint64_t)__double_as_longlong(-INFINITY);
-  wave_scan([&](auto c, auto m) __attribute__((always_inline)) {
-    constexpr int C = decltype(c)::value, RM = decltype(m)::value;
-    const uint64_t b = (uint64_t)__double_as_longlong(bv);
-    const uint32_t lo = dpp<C, RM>((uint32_t)ninf, (uint32_t)b);
-    const uint32_t hi = dpp<C, RM>((uint32_t)(ninf >> 32), (uint32_t)(b >> 32));
-    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)bi);
-    keep_better(bv, bi, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oi);
-  });
-  bv = __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(bv), 63));
-  bi = __builtin_amdgcn_readlane(bi, 63);
-}
-
 // ---- vector groups -------------------------------------------------------------
 // A vector is handled by a group of TPV threads: one wave (TPV = 64, several
 // vectors per workgroup, no workgroup barriers at all) or the whole 256-thread
@@ -224,9 +210,9 @@ struct Smem {
   // reductions across the waves of a group (two slots, alternating, one barrier each)
   uint32_t ru[2][Grp<TPV>::kGW];
   unsigned long long r64[2][Grp<TPV>::kGW];
-  double rd[2][Grp<TPV>::kGW];
   int ri[2][Grp<TPV>::kGW];
-  float rx[2][Grp<TPV>::kGW];
+  float rx[2][Grp<TPV>::kGW], rf[2][Grp<TPV>::kGW], rf2[2][Grp<TPV>::kGW], rs[2][Grp<TPV>::kGW];
+  unsigned long long r64b[2][Grp<TPV>::kGW];
 };
 
 template <int TPV>
@@ -293,104 +279,174 @@ __device__ __forceinline__ uint32_t grp_excl_scan_u32(uint32_t x, uint32_t &tota
 
 // inclusive prefix of x over the group's threads in order
 template <int TPV>
-__device__ __forceinline__ uint64_t grp_incl_scan_u64(uint64_t x, Smem<TPV> &sm, int &slot) {
-  const uint64_t incl = wave_incl_add_u64(x);
-  if constexpr (TPV == kWave) return incl;
-  if (lane_id() == 63) sm.r64[slot][Grp<TPV>::wave()] = incl;
-  Grp<TPV>::sync();
-  uint64_t before = 0;
-#pragma unroll
-  for (int w = 0; w < Grp<TPV>::kGW; ++w)
-    if (w < Grp<TPV>::wave()) before += sm.r64[slot][w];
-  slot ^= 1;
-  return before + incl;
-}
-
-template <int TPV>
 __device__ __forceinline__ int grp_argmax_f32(float bv, int bi, Smem<TPV> &sm, int &slot) {
   wave_argmax_f32(bv, bi);
   if constexpr (TPV == kWave) return bi;
   if (lane_id() == 0) {
-    sm.rd[slot][Grp<TPV>::wave()] = (double)bv;
+    sm.rs[slot][Grp<TPV>::wave()] = bv;
     sm.ri[slot][Grp<TPV>::wave()] = bi;
   }
   Grp<TPV>::sync();
-  double rv = sm.rd[slot][0];
+  float rv = sm.rs[slot][0];
   int ri = sm.ri[slot][0];
 #pragma unroll
-  for (int w = 1; w < Grp<TPV>::kGW; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
+  for (int w = 1; w < Grp<TPV>::kGW; ++w) keep_better(rv, ri, sm.rs[slot][w], sm.ri[slot][w]);
   slot ^= 1;
   return ri;
 }
 
-template <int TPV>
-__device__ __forceinline__ int grp_argmax_f64(double bv, int bi, Smem<TPV> &sm, int &slot) {
-  wave_argmax_f64(bv, bi);
-  if constexpr (TPV == kWave) return bi;
-  if (lane_id() == 0) {
-    sm.rd[slot][Grp<TPV>::wave()] = bv;
-    sm.ri[slot][Grp<TPV>::wave()] = bi;
-  }
-  Grp<TPV>::sync();
-  double rv = sm.rd[slot][0];
-  int ri = sm.ri[slot][0];
-#pragma unroll
-  for (int w = 1; w < Grp<TPV>::kGW; ++w) keep_better(rv, ri, sm.rd[slot][w], sm.ri[slot][w]);
-  slot ^= 1;
-  return ri;
-}
-
-// A draw candidate: its perturbed score s = x + G (fp64, exact), its id and
-// its score x.  Candidates order by (s desc, id asc).
+// A draw candidate: its perturbed score s = x + G (fp32), its id and its
+// score x.  Candidates order by (s desc, id asc).
 struct Cand {
-  double s;
+  float s;
   int id;
   float x;
 };
 
-__device__ __forceinline__ void keep_cand(Cand &b, double s, int id, float x) {
+__device__ __forceinline__ void keep_cand(Cand &b, float s, int id, float x) {
   if (s > b.s || (s == b.s && id < b.id)) b = {s, id, x};
 }
 
-// One group reduction of both a 64-bit sum and the best candidate (a single
-// barrier for a workgroup group); every thread gets both.
+// One group reduction of a float sum (fixed order: the same result on every
+// call with the same inputs) and of the best candidate: a single barrier for
+// a workgroup group; every thread gets both.
 template <int TPV>
-__device__ __forceinline__ Cand grp_sum_and_best(uint64_t &sum, Cand c, Smem<TPV> &sm, int &slot) {
-  const uint64_t ninf = (uint64_t)__double_as_longlong(-INFINITY);
+__device__ __forceinline__ Cand grp_fsum_and_best(float &sum, Cand c, Smem<TPV> &sm, int &slot) {
   wave_scan([&](auto cc, auto m) __attribute__((always_inline)) {
     constexpr int C = decltype(cc)::value, RM = decltype(m)::value;
-    const uint32_t slo = dpp<C, RM>(0u, (uint32_t)sum), shi = dpp<C, RM>(0u, (uint32_t)(sum >> 32));
-    const uint64_t b = (uint64_t)__double_as_longlong(c.s);
-    const uint32_t lo = dpp<C, RM>((uint32_t)ninf, (uint32_t)b);
-    const uint32_t hi = dpp<C, RM>((uint32_t)(ninf >> 32), (uint32_t)(b >> 32));
+    const float os = __uint_as_float(dpp<C, RM>(0u, __float_as_uint(sum)));
+    const float ov = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.s)));
     const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)c.id);
     const float ox = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.x)));
-    sum += ((uint64_t)shi << 32) | slo;
-    keep_cand(c, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oi, ox);
+    sum += os;
+    keep_cand(c, ov, oi, ox);
   });
-  sum = readlane_u64(sum, 63);
-  c.s = __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(c.s), 63));
+  sum = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(sum), 63));
+  c.s = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.s), 63));
   c.id = __builtin_amdgcn_readlane(c.id, 63);
   c.x = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.x), 63));
   if constexpr (TPV == kWave) return c;
   if (lane_id() == 0) {
     const int w = Grp<TPV>::wave();
-    sm.r64[slot][w] = sum;
-    sm.rd[slot][w] = c.s;
+    sm.rf[slot][w] = sum;
+    sm.rs[slot][w] = c.s;
     sm.ri[slot][w] = c.id;
     sm.rx[slot][w] = c.x;
   }
   Grp<TPV>::sync();
-  uint64_t t = 0;
+  float t = 0.0f;
   Cand r = {-INFINITY, INT32_MAX, -INFINITY};
 #pragma unroll
   for (int w = 0; w < Grp<TPV>::kGW; ++w) {
-    t += sm.r64[slot][w];
-    keep_cand(r, sm.rd[slot][w], sm.ri[slot][w], sm.rx[slot][w]);
+    t += sm.rf[slot][w];
+    keep_cand(r, sm.rs[slot][w], sm.ri[slot][w], sm.rx[slot][w]);
   }
   slot ^= 1;
   sum = t;
   return r;
+}
+
+// The largest order key and the best candidate in one group reduction.
+template <int TPV>
+__device__ __forceinline__ Cand grp_max_and_best(uint32_t &mk, Cand c, Smem<TPV> &sm, int &slot) {
+  wave_scan([&](auto cc, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(cc)::value, RM = decltype(m)::value;
+    const uint32_t ok = dpp<C, RM>(0u, mk);
+    const float ov = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.s)));
+    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)c.id);
+    const float ox = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.x)));
+    mk = ok > mk ? ok : mk;
+    keep_cand(c, ov, oi, ox);
+  });
+  mk = (uint32_t)__builtin_amdgcn_readlane((int)mk, 63);
+  c.s = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.s), 63));
+  c.id = __builtin_amdgcn_readlane(c.id, 63);
+  c.x = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.x), 63));
+  if constexpr (TPV == kWave) return c;
+  if (lane_id() == 0) {
+    const int w = Grp<TPV>::wave();
+    sm.ru[slot][w] = mk;
+    sm.rs[slot][w] = c.s;
+    sm.ri[slot][w] = c.id;
+    sm.rx[slot][w] = c.x;
+  }
+  Grp<TPV>::sync();
+  uint32_t t = 0;
+  Cand r = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) {
+    t = sm.ru[slot][w] > t ? sm.ru[slot][w] : t;
+    keep_cand(r, sm.rs[slot][w], sm.ri[slot][w], sm.rx[slot][w]);
+  }
+  slot ^= 1;
+  mk = t;
+  return r;
+}
+
+// Two float sums (fixed order) and the best candidate in one group reduction.
+template <int TPV>
+__device__ __forceinline__ Cand grp_fsum2_and_best(float &a, float &b, Cand c, Smem<TPV> &sm,
+                                                   int &slot) {
+  wave_scan([&](auto cc, auto m) __attribute__((always_inline)) {
+    constexpr int C = decltype(cc)::value, RM = decltype(m)::value;
+    const float oa = __uint_as_float(dpp<C, RM>(0u, __float_as_uint(a)));
+    const float ob = __uint_as_float(dpp<C, RM>(0u, __float_as_uint(b)));
+    const float ov = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.s)));
+    const int oi = (int)dpp<C, RM>((uint32_t)INT32_MAX, (uint32_t)c.id);
+    const float ox = __uint_as_float(dpp<C, RM>(__float_as_uint(-INFINITY), __float_as_uint(c.x)));
+    a += oa;
+    b += ob;
+    keep_cand(c, ov, oi, ox);
+  });
+  a = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(a), 63));
+  b = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(b), 63));
+  c.s = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.s), 63));
+  c.id = __builtin_amdgcn_readlane(c.id, 63);
+  c.x = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(c.x), 63));
+  if constexpr (TPV == kWave) return c;
+  if (lane_id() == 0) {
+    const int w = Grp<TPV>::wave();
+    sm.rf[slot][w] = a;
+    sm.rf2[slot][w] = b;
+    sm.rs[slot][w] = c.s;
+    sm.ri[slot][w] = c.id;
+    sm.rx[slot][w] = c.x;
+  }
+  Grp<TPV>::sync();
+  float ta = 0.0f, tb = 0.0f;
+  Cand r = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) {
+    ta += sm.rf[slot][w];
+    tb += sm.rf2[slot][w];
+    keep_cand(r, sm.rs[slot][w], sm.ri[slot][w], sm.rx[slot][w]);
+  }
+  slot ^= 1;
+  a = ta;
+  b = tb;
+  return r;
+}
+
+// Two 64-bit sums in one group reduction.
+template <int TPV>
+__device__ __forceinline__ void grp_sum2_u64(uint64_t &a, uint64_t &b, Smem<TPV> &sm, int &slot) {
+  a = readlane_u64(wave_incl_add_u64(a), 63);
+  b = readlane_u64(wave_incl_add_u64(b), 63);
+  if constexpr (TPV == kWave) return;
+  if (lane_id() == 0) {
+    sm.r64[slot][Grp<TPV>::wave()] = a;
+    sm.r64b[slot][Grp<TPV>::wave()] = b;
+  }
+  Grp<TPV>::sync();
+  uint64_t ta = 0, tb = 0;
+#pragma unroll
+  for (int w = 0; w < Grp<TPV>::kGW; ++w) {
+    ta += sm.r64[slot][w];
+    tb += sm.r64b[slot][w];
+  }
+  slot ^= 1;
+  a = ta;
+  b = tb;
 }
 
 // ---- Philox (Salmon, Moraes, Dror, Shaw, SC'11) ------------------------------
@@ -892,56 +948,111 @@ __device__ __forceinline__ uint32_t select_topp(const float (&x)[4 * GPT], uint3
   return keep;
 }
 
-// Draw without a top-k cut, the noise gn of every id drawn already.  The token
-// is the best candidate (s desc, id asc) inside the nucleus, and the nucleus
-// is a prefix of the score order (x desc, id asc): an element is inside iff
-// the mass strictly ahead of it is below the target ceil(p Z).  So test the
-// best candidate c; if it is outside, so is every element behind it, and the
-// next candidate is the best one ahead of c.  Each test is one group sum
-// (mass ahead of c), taken together with the next candidate (best ahead of
-// c).  The first element of the score order has nothing ahead of it, so the
-// loop ends; the sampled candidate is outside with probability 1 - p.
+// Draw without a top-k cut (not greedy).  The token is the best candidate
+// (s = x + G desc, id asc) inside the nucleus, and the nucleus is a prefix of
+// the score order (x desc, id asc): an element is inside iff the mass strictly
+// ahead of it is below p Z (with the fixed-point masses of mass_of, below
+// ceil(p Z)).  So test the best candidate c; if it is outside, so is every
+// element behind it, and the next candidate is the best one ahead of c.  The
+// first candidate comes with the maximum (one group reduction), its test with
+// the total mass (a second one); each further test is one more.  The first
+// element of the score order has nothing ahead of it, so the loop ends.  The
+// sampled candidate is outside with probability 1 - p.
+//
+// The masses of the tests are fp32 (hardware exp2), within a relative 2.5e-6
+// of the fixed-point ones in the sums: a test is decided on them unless the
+// mass ahead is within kNucleusMargin Z of p Z, and then on the fixed-point
+// sums, so that the outcome is always that of the fixed-point rule.
+constexpr float kNucleusMargin = 3e-5f;
+
 template <int GPT, int TPV>
-__device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], const float (&gn)[4 * GPT],
-                                            uint32_t active, float mx, float top_p,
-                                            Smem<TPV> &sm, int &slot) {
+__device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], uint32_t active,
+                                            const NoiseKey &nk, float top_p, Smem<TPV> &sm,
+                                            int &slot) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
-  uint64_t mass[EPL], z = 0;
+  float gn[EPL];
+#pragma unroll
+  for (int q = 0; q < GPT; ++q) {
+    const U32x4 wd = noise_block(nk, (uint32_t)(q * TPV + gt));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gn[4 * q + j] = gumbel_from_word(wd.w[j]);
+  }
+  uint32_t mk = 0;
   Cand c = {-INFINITY, INT32_MAX, -INFINITY};
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    mass[i] = ((active >> i) & 1) ? mass_of(x[i], mx) : 0ull;
-    z += mass[i];
-    if ((active >> i) & 1) keep_cand(c, (double)x[i] + (double)gn[i], id_of<TPV>(i, gt), x[i]);
+    if (!((active >> i) & 1)) continue;
+    const uint32_t key = order_key(x[i]);
+    mk = key > mk ? key : mk;
+    keep_cand(c, x[i] + gn[i], id_of<TPV>(i, gt), x[i]);
   }
-  c = grp_sum_and_best<TPV>(z, c, sm, slot);
+  c = grp_max_and_best<TPV>(mk, c, sm, slot);
   if (!(top_p < 1.0f)) return c.id;
-  uint64_t target = (uint64_t)ceil((double)top_p * (double)z);
-  if (target < 1) target = 1;
-  if (target > z) return c.id;
+  const float mx = key_to_float(mk);
+  auto ahead = [&](int i, const Cand &o) __attribute__((always_inline)) {
+    const int id = id_of<TPV>(i, gt);
+    return ((active >> i) & 1) && ((x[i] > o.x) | ((x[i] == o.x) & (id < o.id)));
+  };
+  // fp32 mass, recomputed in each pass (three instructions) rather than held
+  auto mass_f = [&](int i) __attribute__((always_inline)) {
+    return __builtin_amdgcn_exp2f((x[i] - mx) * 1.4426950408889634f);
+  };
+  float zf = 0.0f, af = 0.0f;
+  Cand nc = {-INFINITY, INT32_MAX, -INFINITY};
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const float m = ((active >> i) & 1) ? mass_f(i) : 0.0f;
+    zf += m;
+    if (ahead(i, c)) {
+      af += m;
+      keep_cand(nc, x[i] + gn[i], id_of<TPV>(i, gt), x[i]);
+    }
+  }
+  nc = grp_fsum2_and_best<TPV>(zf, af, nc, sm, slot);
+  const float pz = top_p * zf, margin = kNucleusMargin * zf;
   for (;;) {   // group-uniform
-    uint64_t a = 0;
-    Cand nc = {-INFINITY, INT32_MAX, -INFINITY};
+    bool inside = af < pz;
+    if (fabsf(af - pz) <= margin) {
+      // near the cut: the fixed-point rule, mass ahead of c < ceil(p Z)
+      // (one element after the other: the empty asm statements keep their
+      // order, so that the masses are not all live at once)
+      uint64_t z = 0, a = 0;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        if (!((active >> i) & 1)) continue;
+        float xi = x[i];
+        asm volatile("" : "+v"(xi));
+        const uint64_t m = mass_of(xi, mx);
+        z += m;
+        if (ahead(i, c)) a += m;
+        asm volatile("" : "+v"(z), "+v"(a));
+      }
+      grp_sum2_u64<TPV>(z, a, sm, slot);
+      uint64_t target = (uint64_t)ceil((double)top_p * (double)z);
+      if (target < 1) target = 1;
+      inside = a < target;
+    }
+    if (inside) return c.id;
+    // c is outside: test the best candidate ahead of it
+    c = nc;
+    af = 0.0f;
+    nc = {-INFINITY, INT32_MAX, -INFINITY};
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
-      const int id = id_of<TPV>(i, gt);
-      if (((active >> i) & 1) && ((x[i] > c.x) | ((x[i] == c.x) & (id < c.id)))) {
-        a += mass[i];
-        keep_cand(nc, (double)x[i] + (double)gn[i], id, x[i]);
+      if (ahead(i, c)) {
+        af += mass_f(i);
+        keep_cand(nc, x[i] + gn[i], id_of<TPV>(i, gt), x[i]);
       }
     }
-    nc = grp_sum_and_best<TPV>(a, nc, sm, slot);
-    if (a < target) return c.id;
-    c = nc;
+    nc = grp_fsum_and_best<TPV>(af, nc, sm, slot);
   }
 }
 
 template <int GPT, int TPV>
 __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
                                                uint32_t active, int V, bool greedy, int top_k,
-                                               float top_p, bool pre, Smem<TPV> &sm,
-                                               int &slot) {
+                                               float top_p, Smem<TPV> &sm, int &slot) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
   uint32_t mk = 0;
@@ -967,17 +1078,6 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
   const float mx = key_to_float(mk);
   // the noise key, published by the barrier of the maximum
   const NoiseKey nk{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
-  if (pre) {
-    // the noise of every id (the candidates are tested in perturbed-score order)
-    float gn[EPL];
-#pragma unroll
-    for (int q = 0; q < GPT; ++q) {
-      const U32x4 wd = noise_block(nk, (uint32_t)(q * TPV + gt));
-#pragma unroll
-      for (int j = 0; j < 4; ++j) gn[4 * q + j] = gumbel_from_word(wd.w[j]);
-    }
-    return draw_nucleus<GPT, TPV>(x, gn, active, mx, top_p, sm, slot);
-  }
   int pass = 0;
   bool u_dirty = false;
   uint32_t kept = active;
@@ -985,7 +1085,7 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     kept = select_topk<GPT, TPV>(x, kept, mx, top_k, sm, slot, pass, V, u_dirty);
   if (top_p < 1.0f) kept = select_topp<GPT, TPV>(x, kept, mx, top_p, sm, slot, pass, u_dirty);
   // Gumbel-max over the kept ids, one Philox block per group of four ids
-  double bv = -INFINITY;
+  float bv = -INFINITY;
   int bi = INT32_MAX;
   auto draw = [&](int g, uint32_t bits, float x0, float x1, float x2, float x3)
                   __attribute__((always_inline)) {
@@ -993,7 +1093,7 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     const float xs[4] = {x0, x1, x2, x3};
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      if ((bits >> j) & 1) keep_better(bv, bi, (double)xs[j] + (double)gumbel_from_word(w.w[j]), 4 * g + j);
+      if ((bits >> j) & 1) keep_better(bv, bi, xs[j] + gumbel_from_word(w.w[j]), 4 * g + j);
   };
   // The groups with kept ids move to an LDS list and are dealt to the threads
   // in turn, so that the threads run the same number of Philox blocks, up to one.
@@ -1017,7 +1117,7 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     const DrawItem it = dl[e];
     draw(it.g, it.bits, it.x[0], it.x[1], it.x[2], it.x[3]);
   }
-  return grp_argmax_f64<TPV>(bv, bi, sm, slot);
+  return grp_argmax_f32<TPV>(bv, bi, sm, slot);
 }
 
 // One vector per group of TPV threads: 256 / TPV vectors per workgroup.
@@ -1125,11 +1225,8 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     if (bad) {
       if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
-      // Without a top-k cut the draw tests candidates in perturbed-score order
-      // against the nucleus, which takes the noise of every id.
-      const bool pre = T != 0.0f && !(top_k > 0 && top_k < V);
       // The vector's noise key: 64-bit multiplies on uniform values (scalar
-      // unit), so one wave computes it for the group.
+      // unit); one wave derives it for the group and publishes it in LDS.
       if (T != 0.0f && Grp<TPV>::wave() == 0) {
         const NoiseKey nk = noise_key(sv.seed, rkey, t, k);
         if (lane_id() == 0) {
@@ -1140,7 +1237,15 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
           sm.nkw[4] = nk.c3;
         }
       }
-      token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, pre, sm, slot);
+      if (T != 0.0f && !(top_k > 0 && top_k < V)) {
+        // no top-k cut: candidates in perturbed-score order tested against the
+        // nucleus (the noise of every id, drawn once the key is published)
+        Grp<TPV>::sync();
+        const NoiseKey nk{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
+        token = draw_nucleus<GPT, TPV>(x, active, nk, P, sm, slot);
+      } else {
+        token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, sm, slot);
+      }
       sampled = true;
     }
   }
