@@ -47,8 +47,8 @@ MEASURED_TRAFFIC = {
     # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
     "weight_streaming": dict(
         sources=["k_stream.hip", "gemm_common.h"],
-        sha256="e77f374eb66fb715f2b719a8bbd222fe46cba68ca158988f02f44f0253f1ea34",
-        fetch_bytes=278410679, write_bytes=8388608,
+        sha256="baa3e9fe1109c61e11e76caea374ddc3db2300a2fa640cc3189c6bac0a339913",
+        fetch_bytes=278757581, write_bytes=8388608,
         profile="profiles/head_step_weight_streaming.md"),
 }
 

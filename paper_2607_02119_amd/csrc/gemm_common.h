@@ -28,10 +28,22 @@ __device__ __forceinline__ void static_for(F &&f) {
   }
 }
 
+// Uniform load through the constant address space: a scalar load, counted
+// apart from the vector-memory counter, so it never waits for the global->LDS
+// copies in flight.  Only for buffers that no kernel writes while it runs.
+template <typename T>
+__device__ __forceinline__ T ld_const(const T *p, int i) {
+  return ((const __attribute__((address_space(4))) T *)p)[i];
+}
+
+// The plan header matches the step.  Scalar loads, every word read (no
+// short-circuit), so that they go out together.
 __device__ inline bool plan_ok(const StepView &sv) {
   const int32_t *p = sv.plan;
-  return p[kPlanMagicWord] == kPlanMagic && p[kPlanR] == sv.R && p[kPlanPairs] == sv.n_pairs &&
-         p[kPlanSolo] == sv.n_solo && p[kPlanText] == sv.n_text;
+  const bool magic = ld_const(p, kPlanMagicWord) == kPlanMagic;
+  const bool r = ld_const(p, kPlanR) == sv.R, pairs = ld_const(p, kPlanPairs) == sv.n_pairs;
+  const bool solo = ld_const(p, kPlanSolo) == sv.n_solo, text = ld_const(p, kPlanText) == sv.n_text;
+  return magic & r & pairs & solo & text;
 }
 
 __device__ inline void better(float &bv, int &bi, float v, int i) {
@@ -76,38 +88,46 @@ __device__ __forceinline__ void block_barrier_no_vmem_wait() {
 
 // Epilogue parameters of GEMM rows g0 (even) and g0 + 1: {w, 1/T, out, -2} for
 // a CFG pair (the Main row carries w and T), {1/T0, 1/T1, out0, out1} for solo
-// rows (out -1: no such row).
-__device__ inline float4 pair_params(const StepView &sv, const int32_t *rows, int g0) {
+// rows (out -1: no such row).  In two halves: the loads (at clamped indices,
+// no branch on the loaded parameters, so nothing waits for them yet), and the
+// arithmetic, which may come much later.
+struct PairLoads {
+  float w, t0, t1;
+  int g0;
+  bool ok0, ok1;
+};
+
+// r0, r1: the plan rows of GEMM rows g0 and g0 + 1 (each index clamped to Mg - 1)
+__device__ inline PairLoads pair_params_load(const StepView &sv, int g0, int r0, int r1) {
+  const bool pair = g0 < 2 * sv.n_pairs;
+  const bool ok0 = g0 < sv.Mg && r0 >= 0 && r0 < sv.R;
+  const bool ok1 = !pair && g0 + 1 < sv.Mg && r1 >= 0 && r1 < sv.R;
+  const int c0 = ok0 ? r0 : 0, c1 = ok1 ? r1 : 0;
+  return PairLoads{sv.cfg_w[c0], sv.temperature[c0], sv.temperature[c1], g0, ok0, ok1};
+}
+
+__device__ inline float4 pair_params_finish(const StepView &sv, const PairLoads &p) {
+  auto inv = [](float T) __attribute__((always_inline)) { return T > 0.0f ? 1.0f / T : 1.0f; };
   float4 pr = make_float4(0.0f, 1.0f, __int_as_float(-1), __int_as_float(-1));
-  if (g0 < 2 * sv.n_pairs) {
-    const int r = rows[g0];
-    if (r >= 0 && r < sv.R) {
-      const float T = sv.temperature[r];
-      pr = make_float4(sv.cfg_w[r], T > 0.0f ? 1.0f / T : 1.0f, __int_as_float(g0 >> 1),
-                       __int_as_float(-2));
-    }
+  if (p.g0 < 2 * sv.n_pairs) {
+    if (p.ok0) pr = make_float4(p.w, inv(p.t0), __int_as_float(p.g0 >> 1), __int_as_float(-2));
     return pr;
   }
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int g = g0 + h;
-    if (g < sv.Mg) {
-      const int r = rows[g];
-      if (r >= 0 && r < sv.R) {
-        const float T = sv.temperature[r];
-        const float it = T > 0.0f ? 1.0f / T : 1.0f;
-        const int out = sv.n_pairs + (g - 2 * sv.n_pairs);
-        if (h == 0) {
-          pr.x = it;
-          pr.z = __int_as_float(out);
-        } else {
-          pr.y = it;
-          pr.w = __int_as_float(out);
-        }
-      }
-    }
+  const int out0 = sv.n_pairs + (p.g0 - 2 * sv.n_pairs);
+  if (p.ok0) {
+    pr.x = inv(p.t0);
+    pr.z = __int_as_float(out0);
+  }
+  if (p.ok1) {
+    pr.y = inv(p.t1);
+    pr.w = __int_as_float(out0 + 1);
   }
   return pr;
+}
+
+__device__ inline float4 pair_params(const StepView &sv, const int32_t *rows, int g0) {
+  const int r0 = rows[min(g0, sv.Mg - 1)], r1 = rows[min(g0 + 1, sv.Mg - 1)];
+  return pair_params_finish(sv, pair_params_load(sv, g0, r0, r1));
 }
 
 // Second phase of the LDS epilogue of a BM x BN tile whose sums sit in C

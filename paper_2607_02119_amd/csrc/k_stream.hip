@@ -133,26 +133,40 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     return;
   }
 
+  // The hidden-state waves gather their rows through the plan and start their
+  // copies as soon as the row indices are in.  The per-row epilogue parameters
+  // are loaded before the copies (in order, they complete before them, so the
+  // loop's copy counts stay valid) and staged in LDS after the loop.
+  const int q2 = tid - 128;
+  PairLoads praw{0.0f, 0.0f, 0.0f, 0, false, false};
   if (!w_copier) {
-    // The hidden-state waves gather their rows through the plan, stage the
-    // per-row epilogue parameters in LDS, and wait for all of it before their
-    // first copy, so that only copies are outstanding in their loop counters.
+    // all row loads first (the copy sources and, for the epilogue, the rows of
+    // a GEMM row pair per thread), then the checks: their round trips overlap
+    int prow[QN];
+    static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      prow[q] = 0;
+      if (q < AIA) prow[q] = rows[min(m0 + ((wave_s - 2) * AIA + q) * 8 + seg_r, M - 1)];
+    });
+    const int g0 = m0 + 2 * min(q2, BM / 2 - 1);
+    int pr0 = 0, pr1 = 0;
+    if constexpr (!TEXT) {
+      pr0 = rows[min(g0, sv.Mg - 1)];
+      pr1 = rows[min(g0 + 1, sv.Mg - 1)];
+    }
+    bool bad = false;
     static_for<0, QN>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       src[q] = nullptr;
       if (q < AIA) {
         const int r = ((wave_s - 2) * AIA + q) * 8 + seg_r;
-        int pr = rows[min(m0 + r, M - 1)];
-        if (pr < 0 || pr >= sv.R) {
-          atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-          pr = 0;
-        }
-        src[q] = X + (size_t)pr * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
+        const bool ok = prow[q] >= 0 && prow[q] < sv.R;
+        bad |= !ok;
+        src[q] = X + (size_t)(ok ? prow[q] : 0) * H + ((seg_c ^ ((r >> 1) & 7)) * 8);
       }
     });
-    const int q2 = tid - 128;
-    if (!TEXT && q2 < BM / 2) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
-    wait_vmem_and_lds<0>();
+    if constexpr (!TEXT) praw = pair_params_load(sv, g0, pr0, pr1);
+    if (bad) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
 #pragma unroll
     for (int st = 0; st < SA - 1; ++st) issue_a(st);
   }
@@ -212,6 +226,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // the copies are invisible to the compiler: drain them before reusing LDS
   wait_vmem_and_lds<0>();
   __syncthreads();
+  if (!TEXT && !w_copier && q2 < BM / 2) rowp[q2] = pair_params_finish(sv, praw);
 
   // Epilogue, in two phases through LDS (the rings are free now).
   // Phase 1: every wave writes its partial sums (its k half) to C[kh][row][col].
