@@ -988,6 +988,8 @@ __device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], uint32_t 
     keep_cand(c, x[i] + gn[i], id_of<TPV>(i, gt), x[i]);
   }
   c = grp_max_and_best<TPV>(mk, c, sm, slot);
+  // no orderable candidate (every score NaN): the lowest id
+  if (c.id == INT32_MAX) return 0;
   if (!(top_p < 1.0f)) return c.id;
   const float mx = key_to_float(mk);
   auto ahead = [&](int i, const Cand &o) __attribute__((always_inline)) {
@@ -1033,8 +1035,10 @@ __device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], uint32_t 
       if (target < 1) target = 1;
       inside = a < target;
     }
-    if (inside) return c.id;
-    // c is outside: test the best candidate ahead of it
+    // nothing ahead of c (reached only if the masses are not finite): c
+    if (inside || nc.id == INT32_MAX) return c.id;
+    // c is outside: test the best candidate ahead of it, strictly earlier in
+    // the score order, so the loop ends after at most V tests
     c = nc;
     af = 0.0f;
     nc = {-INFINITY, INT32_MAX, -INFINITY};

@@ -238,6 +238,34 @@ def test_sampler_exact_nucleus_boundary(V, K, Rs, top_p):
     assert tc.exempt["topp"] == 0
 
 
+@pytest.mark.parametrize("tpv_path", ["workgroup", "wave"])
+def test_sampler_non_finite_scores_give_valid_ids(tpv_path):
+    """Scores with NaN and infinities (an overflowing or broken head): the draw
+    without a top-k cut still ends (its candidate loop moves strictly ahead in
+    the score order) and returns an id of the vocabulary.  No parity: the
+    oracle does not define these inputs."""
+    V, K, Rs = (4096, 4, 4) if tpv_path == "workgroup" else (512, 8, 128)
+    wl = inputs.Workload("sampler", H=64, K=K, V=V, n_pairs=0, n_solo=Rs, temperature=1.0,
+                         top_k=0, top_p=0.9, steps=3 * K)
+    say(f"case non-finite scores V={V} K={K} Rs={Rs}")
+    dw = harness.DeviceWorkload(wl, weights=dict(H=64, K=K, V=V, pad_id=V,
+                                                 delays=np.arange(K, dtype=np.int32),
+                                                 W=np.zeros((K, V, 64), np.uint16), bias=None,
+                                                 W_text=None))
+    t = K - 1                                # every codebook has a frame
+    sc = inputs.make_scores(Rs, wl.N, t, sigma=2.0)
+    sc[0, :V] = np.nan                       # every score NaN
+    sc[1, :V:7] = np.nan                     # some NaN
+    sc[2, :V] = -np.inf                      # every score -inf
+    sc[3, V:2 * V:5] = np.inf                # some +inf
+    dw.tokens.fill_(-1)
+    dw.sample_only(t, harness.to_device(np.ascontiguousarray(sc, dtype=np.float32)))
+    torch.cuda.synchronize()
+    g = _cpu(dw.tokens)
+    for r, _ in dw.plan.sampled_rows():
+        assert np.all((g[r] >= 0) & (g[r] < V)), g[r]
+
+
 def test_interleave_roundtrip_on_device():
     rng = np.random.default_rng(0)
     for n_req, K, F, dmax in [(3, 4, 29, 3), (5, 8, 249, 7), (2, 3, 0, 2), (4, 5, 17, 9)]:
