@@ -112,6 +112,9 @@ RAGGED = [
     # at least 256 tiles of 256 x 256: the wide-tile kernel, ragged N and V % 4 != 0
     ("mfma_wide_tiles", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, dtype="bf16",
                              top_k=15, temperature=0.8, steps=10, shuffle=True)),
+    # 2 x 128 tiles of 256 x 128 with a ragged last column tile (V % 4 != 0)
+    ("mfma_ragged_columns", dict(H=256, K=4, V=4093, n_pairs=140, n_solo=20, dtype="bf16",
+                                 top_k=10, temperature=0.9, steps=3, shuffle=True)),
     ("mfma_text_rows", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=300,
                             dtype="bf16", top_k=5, steps=3, shuffle=True)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
@@ -135,6 +138,27 @@ def test_ragged_shapes_every_step(name, kw):
     for t in range(wl.steps):
         _check_step(dw, t, tc, score_tol=tol)
     tc.assert_ok(name)
+    assert dw.status() == 0
+
+
+def test_wide_tiles_over_more_than_one_wave_of_the_chip():
+    """3 x 100 tiles of 256 x 256: more tiles than compute units, so a second
+    round of workgroups runs after the first.  The oracle checks rows of every
+    row tile (pairs and solo rows)."""
+    wl = inputs.Workload("wide_tiles_waves", H=128, K=8, V=3199, n_pairs=300, n_solo=40,
+                         dtype="bf16", top_p=0.9, cfg_w=2.5, steps=9, shuffle=True)
+    say(f"case wide_tiles_waves R={wl.R} Mg={2 * wl.n_pairs + wl.n_solo} N={wl.N}")
+    dw = harness.DeviceWorkload(wl)
+    dw.load_hidden()
+    sr = list(dw.plan.sampled_rows())
+    rows = []
+    for s_ in [0, 1, 64, 127, 128, 200, 255, 256, 299, 300, 319, 339]:
+        r, c = sr[s_]
+        rows += [r] + ([c] if c >= 0 else [])
+    tc = TokenCheck()
+    for t in (0, 8):
+        _check_step(dw, t, tc, rows=sorted(rows), score_tol=1e-2)
+    tc.assert_ok("wide_tiles_waves")
     assert dw.status() == 0
 
 
