@@ -164,7 +164,8 @@ __device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const Step
     auto put = [&](int out, const floatx4 &v) __attribute__((always_inline)) {
       float *dst = sv.scores + (size_t)out * N + nc;
       if (vec_ok) {
-        *reinterpret_cast<floatx4 *>(dst) = v;
+        // streaming store: the scores are read once, by the sampler
+        __builtin_nontemporal_store(v, reinterpret_cast<floatx4 *>(dst));
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
