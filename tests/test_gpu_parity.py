@@ -103,6 +103,13 @@ RAGGED = [
                          dtype="bf16", top_p=0.9, cfg_w=2.0, steps=4, shuffle=True)),
     ("stream_bm128", dict(H=768, K=4, V=129, n_pairs=55, n_solo=3, n_text=100, V_text=515,
                           dtype="bf16", top_k=20, steps=5)),
+    # more than one round of 128-column tiles: 256-column streaming tiles with
+    # a ragged last tile (audio: 64-row tiles, N % 4 != 0; text: 32-row tiles)
+    ("stream_wide_bm64", dict(H=128, K=9, V=3739, n_pairs=20, n_solo=3, n_text=5, V_text=33000,
+                              dtype="bf16", top_k=20, temperature=0.9, steps=10, shuffle=True)),
+    # 128-row 256-column tiles, fewer slices than weight stages (H = 192)
+    ("stream_wide_bm128", dict(H=192, K=9, V=3700, n_pairs=60, n_solo=5, n_text=100,
+                               V_text=40000, dtype="bf16", top_p=0.9, cfg_w=2.5, steps=10)),
     # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
     ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
                                 temperature=0.9, steps=4, shuffle=True)),
