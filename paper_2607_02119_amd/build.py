@@ -18,7 +18,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmcd.so")
 ARCH = "gfx950"
 
-SOURCES = ["mcd_api.cpp", "k_head_gemm.hip", "k_stream.hip", "k_mfma.hip", "k_sample.hip",
+SOURCES = ["mcd_api.cpp", "k_head_gemm.hip", "k_stream.hip", "k_mfma.hip", "k_fused.hip", "k_sample.hip",
            "k_grid.hip"]
 
 COMMON = [

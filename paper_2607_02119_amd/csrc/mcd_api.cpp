@@ -286,14 +286,17 @@ size_t mcd_workspace_bytes(const mcd_head *h, int32_t R) {
 
 namespace {
 
-// K1 for one batch.  Audio and text rows together: the audio projection on the
-// caller's stream and the text projection on the head's second stream, both
-// after everything already on the caller's stream, which waits for both.
+// K1 for one batch.  Audio and text rows together: one launch of both when
+// the batch has that shape, else the audio projection on the caller's stream
+// and the text projection on the head's second stream, both after everything
+// already on the caller's stream, which waits for both.
 hipError_t run_head_gemm(const mcd_head *h, const mcd::StepView &sv, hipStream_t stream) {
   if (h->hv.dtype != MCD_BF16 || sv.Mg == 0 || sv.n_text == 0)
     return mcd::launch_head_gemm(h->hv, sv, stream);
+  bool fused = false;
+  hipError_t e = mcd::launch_mixed_gemm(h->hv, sv, stream, &fused);
+  if (fused || e != hipSuccess) return e;
   std::lock_guard<std::mutex> lock(h->side_mu);
-  hipError_t e = hipSuccess;
   if (!h->side) {
     e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);

@@ -72,6 +72,11 @@ hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
                               hipStream_t stream);   // at most 128 GEMM rows
 hipError_t launch_mfma_gemm(const HeadView &hv, const StepView &sv, bool text,
                             hipStream_t stream);     // any number of rows
+// A batch of audio rows in 256 x 256 tiles and 65..128 text rows: both
+// projections in one launch; *launched is false (and nothing is launched) for
+// other batches.
+hipError_t launch_mixed_gemm(const HeadView &hv, const StepView &sv, hipStream_t st,
+                             bool *launched);
 hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t stream);
 hipError_t launch_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,

@@ -122,6 +122,14 @@ RAGGED = [
     # 2 x 128 tiles of 256 x 128 with a ragged last column tile (V % 4 != 0)
     ("mfma_ragged_columns", dict(H=256, K=4, V=4093, n_pairs=140, n_solo=20, dtype="bf16",
                                  top_k=10, temperature=0.9, steps=3, shuffle=True)),
+    # one launch for both projections: 256 tiles of 256 x 256 for the audio
+    # rows, then 65..128 text rows in 256-column (or 64-column) streaming tiles
+    ("fused_mixed_wide_text", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, n_text=70,
+                                   V_text=33000, dtype="bf16", top_k=15, temperature=0.8,
+                                   steps=10, shuffle=True)),
+    ("fused_mixed_narrow_text", dict(H=128, K=8, V=4096, n_pairs=130, n_solo=0, n_text=128,
+                                     V_text=515, dtype="bf16", top_p=0.9, cfg_w=2.0, steps=9,
+                                     shuffle=True)),
     ("mfma_text_rows", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=300,
                             dtype="bf16", top_k=5, steps=3, shuffle=True)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
