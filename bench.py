@@ -46,9 +46,9 @@ CSRC = os.path.join(ROOT, "paper_2607_02119_amd", "csrc")
 MEASURED_TRAFFIC = {
     # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
     "weight_streaming": dict(
-        sources=["k_stream.hip", "gemm_common.h"],
-        sha256="baa3e9fe1109c61e11e76caea374ddc3db2300a2fa640cc3189c6bac0a339913",
-        fetch_bytes=278757581, write_bytes=8388608,
+        sources=["k_stream.hip", "stream_tile.h", "gemm_common.h"],
+        sha256="87dab1027e57cc3ff7ac62d89794f12552fb83db4fd0f0a0ace85aa525ce70e3",
+        fetch_bytes=277193933, write_bytes=8388608,
         profile="profiles/head_step_weight_streaming.md"),
 }
 
