@@ -79,6 +79,9 @@ def lib():
         L.orc_interleave.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
         L.orc_interleave.restype = ctypes.c_int32
+        L.orc_next_input.argtypes = [ctypes.c_int32] * 6 + [ctypes.c_void_p, ctypes.c_int32] + \
+            [ctypes.c_void_p] * 4
+        L.orc_next_input.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -285,3 +288,30 @@ def sample_rows(head, batch, srow, crow, scores, seed=0, n_slots=0, F_max=0, fra
     if rc:
         raise ValueError("oracle sample_rows: " + ERRORS.get(rc, str(rc)))
     return dict(tokens=tokens, gap=gap, flags=flags, frame_grid=frame_grid)
+
+
+def next_input(E, tokens, row_kind, pad_id, E_text=None):
+    """Next-step input of every row (Sec. 2.1): sum over streams k of
+    E[k][tokens[r][k]] (row V of stream k's table for the pad id), exact in
+    fp64 and rounded once to the table type; TEXT rows take
+    E_text[tokens[r][0]].  E: [K][V + 1][H] float32 or uint16 (bf16 bits);
+    tokens: [R][K] int32; row_kind: [R] uint8.  Returns [R][H] of E's type."""
+    E = np.ascontiguousarray(E)
+    K, V1, H = E.shape
+    dtype = BF16 if E.dtype == np.uint16 else F32
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1, K)
+    R = tokens.shape[0]
+    row_kind = np.ascontiguousarray(row_kind, dtype=np.uint8)
+    assert row_kind.shape == (R,)
+    V_text = 0
+    if E_text is not None:
+        E_text = np.ascontiguousarray(E_text)
+        assert E_text.dtype == E.dtype and E_text.shape[1] == H
+        V_text = E_text.shape[0]
+    out = np.zeros((R, H), dtype=E.dtype)
+    rc = lib().orc_next_input(R, H, K, V1 - 1, int(pad_id), dtype, E.ctypes.data, V_text,
+                              _ptr(E_text), row_kind.ctypes.data, tokens.ctypes.data,
+                              out.ctypes.data)
+    if rc:
+        raise ValueError(ERRORS.get(rc, rc))
+    return out

@@ -379,3 +379,77 @@ int32_t orc_interleave(const int32_t *grid, int32_t F, int32_t K, const int32_t 
     }
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Next-step input (Sec. 2.1): the sum of the embeddings of the tokens a row
+ * emitted at this step, one per stream, in fp64, rounded once to the table
+ * type.  A sum of at most 32 values with 8 (bf16) or 24 (fp32) significant bits
+ * is exact in a double when their exponents span at most 40 or 24 bits, which
+ * covers any embedding table of sane scale; then the result is the exact sum
+ * rounded once. */
+
+/* Round a double to the nearest bfloat16 (8 significant bits), ties to even,
+ * directly from the double (no intermediate fp32 rounding). */
+static uint16_t orc_bf16_rne(double x) {
+  float f;
+  uint32_t bits;
+  if (isnan(x)) return 0x7FC0;
+  if (x == 0.0 || isinf(x)) {
+    f = (float)x;
+    memcpy(&bits, &f, sizeof bits);
+    return (uint16_t)(bits >> 16);
+  }
+  int e;
+  (void)frexp(x, &e);            /* |x| = m * 2^e, 0.5 <= m < 1: leading bit 2^(e-1) */
+  int lead = e - 1;
+  if (lead < -126) lead = -126;  /* bf16 subnormals keep the spacing 2^-133 */
+  double ulp = ldexp(1.0, lead - 7);
+  double q = x / ulp;            /* exact: scaling by a power of two */
+  double r = nearbyint(q);       /* the default rounding mode: nearest, ties to even */
+  double y = r * ulp;
+  if (fabs(y) >= ldexp(1.0, 128)) y = x > 0 ? INFINITY : -INFINITY;
+  f = (float)y;                  /* exact: y has at most 8 significant bits */
+  memcpy(&bits, &f, sizeof bits);
+  return (uint16_t)(bits >> 16);
+}
+
+int32_t orc_next_input(int32_t R, int32_t H, int32_t K, int32_t V, int32_t pad_id,
+                       int32_t dtype, const void *E, int32_t V_text, const void *E_text,
+                       const uint8_t *row_kind, const int32_t *tokens, void *out) {
+  if (R < 0 || H < 1 || K < 1 || V < 1 || !E || !row_kind || !tokens || !out)
+    return ORC_E_SHAPE;
+  if (pad_id >= 0 && pad_id < V) return ORC_E_SHAPE;
+  int32_t rc = ORC_OK;
+  double *acc = (double *)malloc(sizeof(double) * (size_t)H);
+  for (int32_t r = 0; r < R; ++r) {
+    for (int32_t h = 0; h < H; ++h) acc[h] = 0.0;
+    if (row_kind[r] == ORC_ROW_TEXT) {
+      int32_t id = tokens[(int64_t)r * K];
+      if (!E_text || id < 0 || id >= V_text) {
+        rc = ORC_E_PARAM;
+      } else {
+        for (int32_t h = 0; h < H; ++h) acc[h] = orc_elem(E_text, dtype, (int64_t)id * H + h);
+      }
+    } else {
+      for (int32_t k = 0; k < K; ++k) {
+        int32_t tok = tokens[(int64_t)r * K + k];
+        int32_t row;
+        if (tok == pad_id) row = V;
+        else if (tok >= 0 && tok < V) row = tok;
+        else {
+          rc = ORC_E_PARAM;
+          continue;
+        }
+        int64_t base = ((int64_t)k * (V + 1) + row) * H;
+        for (int32_t h = 0; h < H; ++h) acc[h] += orc_elem(E, dtype, base + h);
+      }
+    }
+    for (int32_t h = 0; h < H; ++h) {
+      int64_t i = (int64_t)r * H + h;
+      if (dtype == ORC_BF16) ((uint16_t *)out)[i] = orc_bf16_rne(acc[h]);
+      else ((float *)out)[i] = (float)acc[h];   /* C's conversion: nearest, ties to even */
+    }
+  }
+  free(acc);
+  return rc;
+}

@@ -111,6 +111,19 @@ int32_t orc_deinterleave(const int32_t *streams, int32_t T, int32_t K,
 int32_t orc_interleave(const int32_t *grid, int32_t F, int32_t K, const int32_t *delays,
                        int32_t pad_id, int32_t *streams);
 
+/* Next-step input (Sec. 2.1, delay pattern): the backbone's input for the
+ * next step aggregates the embeddings of the K tokens a row emitted at this
+ * step, one per stream (each belongs to its own delayed frame).  Read here as
+ * a sum: out[r][h] = sum_k E[k][row_k][h], row_k = tokens[r][k], or row V of
+ * stream k's table [V + 1][H] for the pad id.  The sum is taken in fp64 (exact
+ * when the values' exponents span at most 40 bits for bf16, 24 for fp32) and
+ * rounded once, to nearest even, to the table type.  TEXT rows take
+ * E_text[tokens[r][0]].  ORC_E_PARAM for a token outside [0, V) that is not
+ * the pad id, or a text id outside [0, V_text); out is then unspecified. */
+int32_t orc_next_input(int32_t R, int32_t H, int32_t K, int32_t V, int32_t pad_id,
+                       int32_t dtype, const void *E, int32_t V_text, const void *E_text,
+                       const uint8_t *row_kind, const int32_t *tokens, void *out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -471,3 +471,91 @@ def test_exact_tie_of_perturbed_scores_goes_to_lowest_id():
             assert tok2 == 0
         found += 1
     assert found >= 10
+
+
+# ---------------------------------------------------------------------------
+# Next-step input (Sec. 2.1): the sum of the K stream embeddings of the tokens
+# a row emitted, pad rows for pad tokens, text rows from the text table.
+
+def _int_tables(K, V, H, dtype):
+    """Small distinct integers (exact in bf16 and fp32) so that a wrong stream,
+    row or column index changes the result."""
+    k, v, h = np.meshgrid(np.arange(K), np.arange(V + 1), np.arange(H), indexing="ij")
+    vals = ((k * 7 + v * 3 + h * 5) % 61 - 30).astype(np.float32)
+    return vals if dtype == "f32" else inputs.bf16_rne_bits(vals)
+
+
+def _as_float(a):
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    return a.astype(np.float32)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_next_input_brute_force_integers(dtype):
+    rng = np.random.default_rng(3)
+    K, V, H, R, pad = 3, 5, 7, 6, 5
+    E = _int_tables(K, V, H, dtype)
+    tokens = rng.integers(0, V, size=(R, K)).astype(np.int32)
+    tokens[1, 2] = pad
+    tokens[4, :] = pad
+    kinds = np.full(R, inputs.ROW_COND, np.uint8)
+    got = _as_float(oracle.next_input(E, tokens, kinds, pad_id=pad))
+    for r in range(R):
+        for hh in range(H):
+            want = 0
+            for kk in range(K):
+                row = V if tokens[r, kk] == pad else int(tokens[r, kk])
+                want += ((kk * 7 + row * 3 + hh * 5) % 61) - 30
+            assert got[r, hh] == want, (r, hh)
+
+
+def test_next_input_pad_and_text_rows():
+    K, V, H = 2, 4, 3
+    E = np.zeros((K, V + 1, H), np.float32)
+    E[0, V] = [1.0, 2.0, 3.0]        # pad embedding of stream 0
+    E[1, V] = [10.0, 20.0, 30.0]     # pad embedding of stream 1
+    E[1, 2] = [0.5, 0.25, 0.125]
+    E_text = np.arange(6 * H, dtype=np.float32).reshape(6, H)
+    tokens = np.array([[V, V], [V, 2], [4, 0]], np.int32)   # row 2: text id 4 (rest ignored)
+    kinds = np.array([0, 2, 3], np.uint8)
+    out = oracle.next_input(E, tokens, kinds, pad_id=V, E_text=E_text)
+    assert out[0].tolist() == [11.0, 22.0, 33.0]
+    assert out[1].tolist() == [1.5, 2.25, 3.125]
+    assert out[2].tolist() == E_text[4].tolist()
+
+
+def test_next_input_rounds_once_to_nearest_even():
+    """bf16: 1 + 2^-8 is a tie between 1 and 1 + 2^-7 and goes to the even 1;
+    (1 + 2^-7) + 2^-8 goes to 1 + 2^-6; 1 + 2^-8 + 2^-30 is above the tie and
+    rounds up, where a pass through fp32 would first round it to the tie and
+    then down.  fp32: the same at 2^-24 (the sum stays exact in fp64)."""
+    one, b8, b30, odd = 0x3F80, 0x3B80, 0x3080, 0x3F81     # 1, 2^-8, 2^-30, 1 + 2^-7
+    E = np.zeros((3, 2, 1), np.uint16)                      # K = 3, V = 1 (+ pad row)
+    cases = [((one, b8, 0), 0x3F80), ((odd, b8, 0), 0x3F82), ((one, b8, b30), 0x3F81),
+             ((one | 0x8000, b8 | 0x8000, 0), 0xBF80)]
+    for (a, b, c), want in cases:
+        E[0, 0, 0], E[1, 0, 0], E[2, 0, 0] = a, b, c
+        out = oracle.next_input(E, np.zeros((1, 3), np.int32), np.zeros(1, np.uint8), pad_id=1)
+        assert int(out[0, 0]) == want, (hex(a), hex(b), hex(c), hex(int(out[0, 0])))
+    F = np.zeros((3, 2, 1), np.float32)
+    for (a, b, c), want in [((1.0, 2.0 ** -24, 0.0), 1.0),
+                            ((1.0 + 2.0 ** -23, 2.0 ** -24, 0.0), 1.0 + 2.0 ** -22),
+                            ((1.0, 2.0 ** -24, 2.0 ** -40), 1.0 + 2.0 ** -23)]:
+        F[0, 0, 0], F[1, 0, 0], F[2, 0, 0] = a, b, c
+        out = oracle.next_input(F, np.zeros((1, 3), np.int32), np.zeros(1, np.uint8), pad_id=1)
+        assert float(out[0, 0]) == want
+
+
+def test_next_input_rejects_bad_tokens():
+    E = np.zeros((2, 4, 2), np.float32)                     # K = 2, V = 3
+    kinds = np.zeros(1, np.uint8)
+    for tok in ([3, 0], [0, -1], [7, 0]):                    # 3 is not the pad id (9)
+        with pytest.raises(ValueError):
+            oracle.next_input(E, np.array([tok], np.int32), kinds, pad_id=9)
+    with pytest.raises(ValueError):                          # pad id inside [0, V)
+        oracle.next_input(E, np.zeros((1, 2), np.int32), kinds, pad_id=2)
+    with pytest.raises(ValueError):                          # text id past the text table
+        oracle.next_input(E, np.array([[5, 0]], np.int32), np.array([3], np.uint8), pad_id=9,
+                          E_text=np.zeros((5, 2), np.float32))
