@@ -82,6 +82,33 @@ def k1_traffic(workload):
     return m["fetch_bytes"] + m["write_bytes"]
 
 
+def graph_per_launch(torch, fn, reps=50, replays=8):
+    """Mean duration of fn(i)'s launch, back to back on the GPU: `reps` calls
+    (i = 0 .. reps - 1) captured in one HIP graph, replayed `replays` times between HIP events, so
+    the host's per-call cost (the ctypes call) is not in the figure.  fn
+    launches on torch's current stream, which is the capture stream while the
+    graph is recorded; it must allocate nothing."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn(0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(reps):
+            fn(i)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(replays):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * replays)
+
+
 def copy_probe(torch):
     """A plain device copy of known size (read and write COPY_PROBE_BYTES each),
     the calibration point for the FETCH_SIZE / WRITE_SIZE counters."""
@@ -139,6 +166,8 @@ def main():
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="weight_streaming")
+    ap.add_argument("--no-next-input", action="store_true",
+                    help="skip the timing of the next-step input kernel")
     ap.add_argument("--weight-copies", type=int, default=0,
                     help="weight copies rotated per step (0: enough to exceed 3x the MALL)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -206,6 +235,25 @@ def main():
     ms_k2 = per_launch(sample)
     status |= dw.status()
 
+    # the next row of the path: the next-step input built from the last
+    # step's tokens (sum of the K stream embeddings per row), timed alone
+    next_input = None
+    if not args.no_next_input:
+        dw.load_embeddings()
+        # a different set of tokens per launch, so that the embedding rows
+        # come from HBM as they do when each step's tokens are new
+        tok_sets = harness.to_device(inputs.make_token_sets(wl, 50, dw.layout))
+        ms_ni = graph_per_launch(torch, lambda i: dw.run_next_input(tok_sets[i]), reps=50)
+        status |= dw.status()
+        esz = 2 if wl.dtype == "bf16" else 4
+        ni_bytes = ((2 * wl.n_pairs + wl.n_solo) * wl.K * wl.H + wl.n_text * wl.H
+                    + wl.R * wl.H) * esz
+        ni_gbs = ni_bytes / (ms_ni * 1e-3) / 1e9
+        next_input = {"kernel": "next_input_kernel (mcd_next_input)", "bound": "hbm",
+                      "us_per_launch": round(ms_ni * 1e3, 2), "algorithmic_bytes": ni_bytes,
+                      "achieved": round(ni_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                      "frac": round(ni_gbs / HBM_PEAK_GBS, 4)}
+
     tokens_per_step = wl.Rs * wl.K
     value = tokens_per_step / (ms_step * 1e-3)
     mfma_bound = alg["flops"] / (BF16_PEAK_TFLOPS * 1e12) > alg["bytes"] / (HBM_PEAK_GBS * 1e9)
@@ -244,6 +292,8 @@ def main():
                  "us_sample_kernel": round(ms_k2 * 1e3, 2),
                  "device_status": status},
     }
+    if next_input is not None:
+        out["next_input"] = next_input
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

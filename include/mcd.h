@@ -64,7 +64,8 @@ enum { MCD_ROW_COND = 0, MCD_ROW_UNCOND = 1, MCD_ROW_SOLO = 2, MCD_ROW_TEXT = 3 
 enum {
   MCD_DEV_BAD_PARAM = 1u,   /* temperature < 0 or NaN, top_p <= 0 or NaN, non-finite w */
   MCD_DEV_GRID_RANGE = 2u,  /* grid_slot >= n_slots or frame >= F_max: cell not written */
-  MCD_DEV_BAD_PLAN = 4u     /* device plan does not match the counts of the call */
+  MCD_DEV_BAD_PLAN = 4u,    /* device plan does not match the counts of the call */
+  MCD_DEV_BAD_TOKEN = 8u    /* mcd_next_input: a token outside its table */
 };
 
 #define MCD_MAX_K 32         /* codebooks per head */
@@ -179,6 +180,39 @@ mcd_status mcd_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, in
 mcd_status mcd_interleave(const int32_t *grid, int32_t n_req, int32_t F, int32_t K,
                           const int32_t *delays /*[host][K]*/, int32_t pad_id,
                           int32_t *streams, hipStream_t stream);
+
+/* ---- next-step input (Sec. 2.1, delay pattern) ----------------------------
+ * The backbone's input for the next step aggregates the embeddings of the K
+ * tokens each row emitted at this step, one per stream (each for its own
+ * delayed frame).  Read as their sum:
+ *   out[r][h] = sum_k E[k][row_k][h],   row_k = tokens[r][k], or V for pad_id;
+ * TEXT rows (row_kind MCD_ROW_TEXT) take E_text[tokens[r][0]][h].  The sum is
+ * formed in fp64 and rounded once, to nearest even, to the table type: the
+ * exact sum rounded once whenever the values' exponents span at most 40 bits
+ * (bf16) or 24 bits (fp32).  After mcd_head_step a Companion row holds its
+ * Main row's tokens, so both get the same input. */
+typedef struct {
+  int32_t R;                 /* rows, >= 0 */
+  int32_t H;                 /* embedding width, >= 1 */
+  int32_t K;                 /* streams, 1..MCD_MAX_K */
+  int32_t V;                 /* audio sub-vocabulary per stream, >= 1 */
+  int32_t pad_id;            /* outside [0, V): selects row V of every stream's table */
+  mcd_dtype dtype;           /* element type of E, E_text and out */
+  const void *E;             /* [K][V + 1][H]; row V of stream k is its pad embedding */
+  int32_t V_text;            /* rows of E_text, 0 if none */
+  const void *E_text;        /* [V_text][H] or NULL */
+  const uint8_t *row_kind;   /* [R] MCD_ROW_* of every row */
+  const int32_t *tokens;     /* [R][K], e.g. the tokens_out of a step */
+  void *out;                 /* [R][H] of dtype; must not overlap the inputs */
+  void *workspace;           /* a step workspace (its status word), or NULL */
+} mcd_next_input_args;
+
+/* Launches on `stream`; no allocation, no synchronisation.  MCD_E_INVALID for
+ * bad sizes, a pad_id inside [0, V), or E, E_text or out not 16-byte aligned.
+ * A token outside [0, V) other than pad_id, a text id outside [0, V_text), or
+ * a TEXT row without a text table makes that row's output zero and sets
+ * MCD_DEV_BAD_TOKEN in the workspace status word (when a workspace is given). */
+mcd_status mcd_next_input(const mcd_next_input_args *args, hipStream_t stream);
 
 /* Synchronises `stream`, returns the status word in *code and clears it. */
 mcd_status mcd_read_device_status(void *workspace, uint32_t *code, hipStream_t stream);

@@ -344,6 +344,41 @@ mcd_status mcd_sample_step(const mcd_head *h, const mcd_step_args *a, hipStream_
   return MCD_OK;
 }
 
+mcd_status mcd_next_input(const mcd_next_input_args *a, hipStream_t stream) {
+  if (!a) return fail(MCD_E_INVALID, "null args");
+  if (a->R < 0 || a->H < 1 || a->K < 1 || a->K > MCD_MAX_K || a->V < 1 || a->V_text < 0)
+    return fail(MCD_E_INVALID, "bad sizes (R=%d H=%d K=%d V=%d V_text=%d)", a->R, a->H, a->K,
+                a->V, a->V_text);
+  if (a->dtype != MCD_F32 && a->dtype != MCD_BF16) return fail(MCD_E_INVALID, "bad dtype");
+  if (a->pad_id >= 0 && a->pad_id < a->V)
+    return fail(MCD_E_INVALID, "pad_id %d is a token id of [0, %d)", a->pad_id, a->V);
+  if ((int64_t)a->K * (a->V + 1) * a->H > ((int64_t)1 << 40))
+    return fail(MCD_E_INVALID, "table too large");
+  if (a->R == 0) return MCD_OK;
+  if (!a->E || !a->out || !a->tokens || !a->row_kind) return fail(MCD_E_INVALID, "null buffer");
+  if ((a->V_text > 0) != (a->E_text != nullptr))
+    return fail(MCD_E_INVALID, "V_text and E_text disagree");
+  if (!aligned(a->E, 16) || !aligned(a->out, 16) || (a->E_text && !aligned(a->E_text, 16)))
+    return fail(MCD_E_INVALID, "E, E_text and out must be 16-byte aligned");
+  if (a->workspace && !aligned(a->workspace, 256))
+    return fail(MCD_E_INVALID, "workspace must be 256-byte aligned");
+  mcd::EmbedView ev;
+  ev.R = a->R;
+  ev.H = a->H;
+  ev.K = a->K;
+  ev.V = a->V;
+  ev.pad_id = a->pad_id;
+  ev.V_text = a->V_text;
+  ev.E = a->E;
+  ev.E_text = a->E_text;
+  ev.row_kind = a->row_kind;
+  ev.tokens = a->tokens;
+  ev.out = a->out;
+  ev.status = reinterpret_cast<uint32_t *>(a->workspace);
+  hipError_t e = mcd::launch_next_input(ev, a->dtype == MCD_BF16, stream);
+  return e == hipSuccess ? MCD_OK : hip_fail(e, "next-input launch");
+}
+
 mcd_status mcd_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,
                             const int32_t *delays, int32_t *grid, hipStream_t stream) {
   if (n_req < 0 || T < 0 || K < 1 || K > MCD_MAX_K) return fail(MCD_E_INVALID, "bad sizes");

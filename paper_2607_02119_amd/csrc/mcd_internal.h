@@ -77,6 +77,16 @@ hipError_t launch_mfma_gemm(const HeadView &hv, const StepView &sv, bool text,
 // other batches.
 hipError_t launch_mixed_gemm(const HeadView &hv, const StepView &sv, hipStream_t st,
                              bool *launched);
+// Next-step input (k_embed.hip): sizes and pointers validated by the caller.
+struct EmbedView {
+  int32_t R, H, K, V, pad_id, V_text;
+  const void *E, *E_text;
+  const uint8_t *row_kind;
+  const int32_t *tokens;
+  void *out;
+  uint32_t *status;          // or null
+};
+hipError_t launch_next_input(const EmbedView &ev, bool bf16, hipStream_t stream);
 hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t stream);
 hipError_t launch_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,

@@ -100,3 +100,21 @@ class DeviceWorkload:
 
     def status(self):
         return mcd.mcd_read_device_status(self.workspace)
+
+    def load_embeddings(self, tables=None):
+        """Upload the next-step input's embedding tables (default: the seeded
+        ones of the workload) and allocate the output."""
+        self.host_emb = tables if tables is not None else inputs.make_embeddings(self.wl)
+        self.E = to_device(self.host_emb["E"], self.device)
+        Et = self.host_emb["E_text"]
+        self.E_text = None if Et is None else to_device(Et, self.device)
+        self.row_kind_dev = to_device(np.ascontiguousarray(self.layout["row_kind"]), self.device)
+        self.next_in = torch.empty((self.wl.R, self.wl.H), dtype=self.E.dtype, device=self.device)
+        return self.next_in
+
+    def run_next_input(self, tokens=None, stream=None):
+        """Next-step input of every row from `tokens` (default: the last step's)."""
+        mcd.mcd_next_input(self.E, self.tokens if tokens is None else tokens, self.row_kind_dev,
+                           self.host_head["pad_id"], self.next_in, E_text=self.E_text,
+                           workspace=self.workspace, stream=stream)
+        return self.next_in

@@ -23,6 +23,9 @@ Recipe (fixed seeds; numpy's PCG64 via ``default_rng``):
     rows, -1 for companion and text rows.
   * every row starts at step 0 and advances by one per step; each request has
     n_frames = steps - max(delay) frames.
+  * embedding tables of the next-step input: E[k] = bf16_rne(N(0,1)) of shape
+    [V + 1][H] from default_rng([seed_e, k]) (row V: the stream's pad
+    embedding), E_text in 4096-row blocks b from default_rng([seed_e, 1000, b]).
 """
 from __future__ import annotations
 
@@ -37,6 +40,7 @@ SEED_SAMPLING = 0
 SEED_W = 1
 SEED_H = 2
 SEED_PERM = 3
+SEED_E = 4
 
 
 @dataclasses.dataclass(frozen=True)
@@ -153,6 +157,37 @@ def make_weights(wl: Workload, seed_w: int = SEED_W) -> dict:
                                        wl.dtype)
     return dict(H=wl.H, K=wl.K, V=wl.V, pad_id=wl.pad, delays=np.array(wl.delay_list, np.int32),
                 W=W, bias=None, W_text=Wt)
+
+
+def make_embeddings(wl: Workload, seed_e: int = SEED_E) -> dict:
+    """Embedding tables of the next-step input: E[K][V + 1][H] (row V of each
+    stream is its pad embedding) and E_text[V_text][H] or None; uint16 bf16
+    bits or float32, like the head."""
+    edt = np.uint16 if wl.dtype == "bf16" else np.float32
+    E = np.empty((wl.K, wl.V + 1, wl.H), dtype=edt)
+    for k in range(wl.K):
+        E[k] = _to_dtype(_normal([seed_e, k], (wl.V + 1, wl.H)), wl.dtype)
+    Et = None
+    if wl.V_text > 0:
+        Et = np.empty((wl.V_text, wl.H), dtype=edt)
+        blk = 4096
+        for b in range(0, wl.V_text, blk):
+            rows = min(blk, wl.V_text - b)
+            Et[b:b + rows] = _to_dtype(_normal([seed_e, 1000, b // blk], (rows, wl.H)), wl.dtype)
+    return dict(E=E, E_text=Et)
+
+
+def make_token_sets(wl: Workload, n: int, layout: dict, seed: int = SEED_E) -> np.ndarray:
+    """n sets of one step's tokens, int32 [n][R][K]: uniform audio ids in
+    [0, V) per stream, a uniform text id in [0, V_text) in column 0 of text
+    rows (the rest 0), from default_rng([seed, 2000])."""
+    rng = np.random.default_rng([seed, 2000])
+    tok = rng.integers(0, wl.V, size=(n, wl.R, wl.K), dtype=np.int32)
+    text = np.asarray(layout["row_kind"]) == ROW_TEXT
+    if text.any():
+        tok[:, text, :] = 0
+        tok[:, text, 0] = rng.integers(0, wl.V_text, size=(n, int(text.sum())), dtype=np.int32)
+    return tok
 
 
 def row_layout(wl: Workload, seed_perm: int = SEED_PERM) -> dict:

@@ -24,7 +24,7 @@ _lib = ctypes.CDLL(_LIB_PATH)
 MCD_OK, MCD_E_INVALID, MCD_E_UNSUPPORTED, MCD_E_WORKSPACE, MCD_E_HIP = range(5)
 MCD_F32, MCD_BF16 = 0, 1
 MCD_ROW_COND, MCD_ROW_UNCOND, MCD_ROW_SOLO, MCD_ROW_TEXT = 0, 1, 2, 3
-MCD_DEV_BAD_PARAM, MCD_DEV_GRID_RANGE, MCD_DEV_BAD_PLAN = 1, 2, 4
+MCD_DEV_BAD_PARAM, MCD_DEV_GRID_RANGE, MCD_DEV_BAD_PLAN, MCD_DEV_BAD_TOKEN = 1, 2, 4, 8
 MCD_MAX_K, MCD_MAX_V = 32, 4096
 
 _vp = ctypes.c_void_p
@@ -50,6 +50,12 @@ class mcd_step_args(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
+class mcd_next_input_args(ctypes.Structure):
+    _fields_ = [("R", _i32), ("H", _i32), ("K", _i32), ("V", _i32), ("pad_id", _i32),
+                ("dtype", ctypes.c_int), ("E", _vp), ("V_text", _i32), ("E_text", _vp),
+                ("row_kind", _vp), ("tokens", _vp), ("out", _vp), ("workspace", _vp)]
+
+
 def _sig(name, res, *args):
     f = getattr(_lib, name)
     f.restype = res
@@ -71,6 +77,7 @@ _mcd_sample_step = _sig("mcd_sample_step", ctypes.c_int, _vp, ctypes.POINTER(mcd
 _mcd_head_logits = _sig("mcd_head_logits", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
 _mcd_deinterleave = _sig("mcd_deinterleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _vp, _vp)
 _mcd_interleave = _sig("mcd_interleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _i32, _vp, _vp)
+_mcd_next_input = _sig("mcd_next_input", ctypes.c_int, ctypes.POINTER(mcd_next_input_args), _vp)
 _mcd_read_device_status = _sig("mcd_read_device_status", ctypes.c_int, _vp,
                                ctypes.POINTER(ctypes.c_uint32), _vp)
 _mcd_status_string = _sig("mcd_status_string", ctypes.c_char_p, ctypes.c_int)
@@ -79,8 +86,8 @@ _mcd_last_error = _sig("mcd_last_error", ctypes.c_char_p)
 EXPORTED = ["mcd_head_create", "mcd_head_destroy", "mcd_plan_words", "mcd_batch_plan",
             "mcd_plan_sampled_row", "mcd_workspace_bytes", "mcd_head_step", "mcd_head_logits",
             "mcd_sample_step",
-            "mcd_deinterleave", "mcd_interleave", "mcd_read_device_status", "mcd_status_string",
-            "mcd_last_error"]
+            "mcd_deinterleave", "mcd_interleave", "mcd_next_input", "mcd_read_device_status",
+            "mcd_status_string", "mcd_last_error"]
 
 
 class McdError(RuntimeError):
@@ -202,6 +209,18 @@ def mcd_interleave(grid, delays, pad_id, streams, stream=None):
     d = np.ascontiguousarray(delays, dtype=np.int32)
     _check(_mcd_interleave(_ptr(grid), n_req, F, K, d.ctypes.data, pad_id, _ptr(streams),
                            _stream(stream)), "mcd_interleave")
+
+
+def mcd_next_input(E, tokens, row_kind, pad_id, out, E_text=None, workspace=None, stream=None):
+    """Next-step input of every row: E [K][V + 1][H] (bf16 or fp32, device),
+    tokens int32 [R][K], row_kind uint8 [R], out [R][H] of E's type (device)."""
+    K, V1, H = E.shape
+    R = tokens.shape[0]
+    dtype = {torch.bfloat16: MCD_BF16, torch.float32: MCD_F32}[E.dtype]
+    a = mcd_next_input_args(R, H, K, V1 - 1, int(pad_id), dtype, _ptr(E),
+                            0 if E_text is None else E_text.shape[0], _ptr(E_text),
+                            _ptr(row_kind), _ptr(tokens), _ptr(out), _ptr(workspace))
+    _check(_mcd_next_input(ctypes.byref(a), _stream(stream)), "mcd_next_input")
 
 
 def mcd_read_device_status(workspace, stream=None):

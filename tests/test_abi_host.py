@@ -114,3 +114,28 @@ def test_interleave_argument_errors():
     mcd._check(mcd._mcd_deinterleave(None, 0, 5, 2, np.array([0, 1], np.int32).ctypes.data,
                                      None, None), "x")
     assert mcd.mcd_status_string(mcd.MCD_E_HIP) == "hip error"
+
+
+def _next_input_args(**kw):
+    a = dict(R=4, H=64, K=3, V=50, pad_id=50, dtype=mcd.MCD_BF16, E=FAKE_W, V_text=0, E_text=None,
+             row_kind=FAKE_W, tokens=FAKE_W, out=FAKE_W * 2, workspace=None)
+    a.update(kw)
+    return mcd.mcd_next_input_args(a["R"], a["H"], a["K"], a["V"], a["pad_id"], a["dtype"], a["E"],
+                                   a["V_text"], a["E_text"], a["row_kind"], a["tokens"], a["out"],
+                                   a["workspace"])
+
+
+def test_next_input_validation():
+    """Rejected before any launch; R = 0 is a no-op."""
+    bad = [dict(R=-1), dict(H=0), dict(K=0), dict(K=33), dict(V=0), dict(V_text=-1),
+           dict(dtype=7), dict(pad_id=0), dict(pad_id=49), dict(E=None), dict(out=None),
+           dict(tokens=None), dict(row_kind=None), dict(E=FAKE_W + 8), dict(out=FAKE_W + 4),
+           dict(V_text=10), dict(E_text=FAKE_W), dict(V_text=10, E_text=FAKE_W + 2),
+           dict(workspace=FAKE_W + 16)]
+    for b in bad:
+        a = _next_input_args(**b)
+        assert mcd._mcd_next_input(ctypes.byref(a), None) == mcd.MCD_E_INVALID, b
+    for ok_empty in (dict(R=0), dict(R=0, E=None, out=None)):
+        a = _next_input_args(**ok_empty)
+        assert mcd._mcd_next_input(ctypes.byref(a), None) == mcd.MCD_OK
+    assert mcd._mcd_next_input(None, None) == mcd.MCD_E_INVALID
