@@ -7,6 +7,9 @@ or de-interleave), and both the HIP path and the CPU oracle consume exactly the
 arrays it returns.
 
 Recipe (fixed seeds; numpy's PCG64 via ``default_rng``):
+  * stream-embedding term of the heads (when a workload asks for it): the fp32
+    bias b[k][v] = N(0,1) from default_rng([seed_w, 2000]), given as it is (the
+    product W_k e_k of a model's stream embedding e_k, precomputed).
   * head weights  W_k = bf16_rne(N(0,1) / sqrt(H)) from default_rng([seed_w, k]),
     i.e. standard deviation 1/sqrt(H) so each logit is ~N(0,1); the text head
     W_text in 4096-row blocks b from default_rng([seed_w, 1000, b]).  fp32
@@ -62,6 +65,7 @@ class Workload:
     shuffle: bool = False
     delays: tuple | None = None  # default d_k = k
     pad_id: int | None = None    # default V
+    bias: bool = False           # stream-embedding term b[k][v] (W_k e_k) of the heads
 
     @property
     def R(self) -> int:
@@ -155,8 +159,11 @@ def make_weights(wl: Workload, seed_w: int = SEED_W) -> dict:
             rows = min(blk, wl.V_text - b)
             Wt[b:b + rows] = _to_dtype(_normal([seed_w, 1000, b // blk], (rows, wl.H)) * scale,
                                        wl.dtype)
+    bias = None
+    if wl.bias:
+        bias = np.ascontiguousarray(_normal([seed_w, 2000], (wl.K, wl.V)))
     return dict(H=wl.H, K=wl.K, V=wl.V, pad_id=wl.pad, delays=np.array(wl.delay_list, np.int32),
-                W=W, bias=None, W_text=Wt)
+                W=W, bias=bias, W_text=Wt)
 
 
 def make_embeddings(wl: Workload, seed_e: int = SEED_E) -> dict:

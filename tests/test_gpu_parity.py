@@ -101,6 +101,18 @@ RAGGED = [
                               dtype="bf16", top_k=7, temperature=0.7, steps=5, shuffle=True)),
     ("stream_bm64", dict(H=512, K=2, V=333, n_pairs=25, n_solo=3, n_text=40, V_text=1000,
                          dtype="bf16", top_p=0.9, cfg_w=2.0, steps=4, shuffle=True)),
+    # the stream-embedding term (a per-codebook bias) on each kernel path
+    ("bias_stream_bm32", dict(H=256, K=3, V=37, n_pairs=10, n_solo=5, n_text=3, V_text=300,
+                              dtype="bf16", top_k=7, temperature=0.7, steps=5, shuffle=True,
+                              bias=True)),
+    ("bias_stream_wide", dict(H=128, K=9, V=3739, n_pairs=20, n_solo=3, dtype="bf16", top_k=20,
+                              steps=10, bias=True)),
+    ("bias_mfma", dict(H=192, K=4, V=256, n_pairs=100, n_solo=100, dtype="bf16", top_p=0.9,
+                       cfg_w=2.5, steps=4, bias=True)),
+    ("bias_fused_mixed", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, n_text=70, V_text=900,
+                              dtype="bf16", top_k=15, steps=10, shuffle=True, bias=True)),
+    ("bias_f32", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70, dtype="f32",
+                      top_k=5, top_p=0.8, steps=5, shuffle=True, bias=True)),
     ("stream_bm128", dict(H=768, K=4, V=129, n_pairs=55, n_solo=3, n_text=100, V_text=515,
                           dtype="bf16", top_k=20, steps=5)),
     # more than one round of 128-column tiles: 256-column streaming tiles with
