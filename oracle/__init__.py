@@ -93,6 +93,7 @@ class StepArgs(ctypes.Structure):
         ("delays", ctypes.c_void_p), ("dtype", ctypes.c_int32),
         ("W", ctypes.c_void_p), ("bias", ctypes.c_void_p),
         ("V_text", ctypes.c_int32), ("W_text", ctypes.c_void_p),
+        ("V_stream", ctypes.c_void_p),
         ("R", ctypes.c_int32), ("hidden", ctypes.c_void_p),
         ("pair_map", ctypes.c_void_p), ("row_kind", ctypes.c_void_p),
         ("cfg_w", ctypes.c_void_p), ("temperature", ctypes.c_void_p),
@@ -211,7 +212,10 @@ def _step_struct(head, batch, seed, n_slots, F_max, tol, keep):
     a = StepArgs()
     H, K, V = head["H"], head["K"], head["V"]
     dtype = BF16 if head["W"].dtype == np.uint16 else F32
-    W = np.ascontiguousarray(head["W"]).reshape(K * V, H)
+    vs = head.get("V_stream")
+    vs = None if vs is None else _c(vs, np.int32)
+    N = K * V if vs is None else int(vs.sum())
+    W = np.ascontiguousarray(head["W"]).reshape(N, H)
     delays = _c(head["delays"], np.int32)
     bias = _c(head.get("bias"), np.float32)
     Wt = head.get("W_text")
@@ -225,7 +229,8 @@ def _step_struct(head, batch, seed, n_slots, F_max, tol, keep):
     arrs = {name: _c(batch[name], dt) for name, dt in cols.items()}
     rk = batch.get("rng_key")
     arrs["rng_key"] = _c(rk, np.uint64)
-    keep += [W, delays, bias, Wt, hidden] + list(arrs.values())
+    keep += [W, delays, bias, Wt, hidden, vs] + list(arrs.values())
+    a.V_stream = _ptr(vs)
     a.H, a.K, a.V, a.pad_id = H, K, V, head["pad_id"]
     a.delays, a.dtype, a.W, a.bias = delays.ctypes.data, dtype, W.ctypes.data, _ptr(bias)
     a.V_text = 0 if Wt is None else Wt.shape[0]
@@ -238,22 +243,35 @@ def _step_struct(head, batch, seed, n_slots, F_max, tol, keep):
     return a
 
 
+def stream_sizes(head):
+    """Ids of every stream: V_stream, or V for each of the K streams."""
+    vs = head.get("V_stream")
+    return [head["V"]] * head["K"] if vs is None else [int(v) for v in vs]
+
+
+def head_columns(head):
+    """N: the columns of all streams together."""
+    return int(sum(stream_sizes(head)))
+
+
 def head_step(head, batch, seed=0, n_slots=0, F_max=0, frame_grid=None,
               gap_tol=1e-3, topk_tol=1e-6, topp_tol=1e-6, want_scores=True):
     """One decode step of the head over a batch (all arrays numpy, host).
 
     head: dict(H, K, V, pad_id, delays[K], W[K][V][H] (float32 or uint16 bf16 bits),
-               bias[K][V] or None, W_text[V_text][H] or None)
+               bias[K][V] or None, W_text[V_text][H] or None; optionally V_stream[K]
+               for streams of unequal size, with W[N][H] and bias[N], N = sum V_stream)
     batch: dict(hidden[R][H], pair_map, row_kind, cfg_w, temperature, top_k, top_p,
                 rng_key or None, step, n_frames, grid_slot)
-    Returns dict(tokens[R][K], scores[R][K*V] (fp64, COND/SOLO rows), gap[R][K], flags[R][K],
+    Returns dict(tokens[R][K], scores[R][N] (fp64, COND/SOLO rows), gap[R][K], flags[R][K],
                  frame_grid) -- frame_grid is updated in place when given.
     """
     keep = []
     a = _step_struct(head, batch, seed, n_slots, F_max, (gap_tol, topk_tol, topp_tol), keep)
-    R, K, V = a.R, a.K, a.V
+    R, K = a.R, a.K
+    N = head_columns(head)
     tokens = np.full((R, K), -1, dtype=np.int32)
-    scores = np.full((R, K * V), np.nan) if want_scores else None
+    scores = np.full((R, N), np.nan) if want_scores else None
     gap = np.full((R, K), np.inf)
     flags = np.zeros((R, K), dtype=np.uint32)
     if frame_grid is not None:
@@ -277,7 +295,7 @@ def sample_rows(head, batch, srow, crow, scores, seed=0, n_slots=0, F_max=0, fra
     srow = np.ascontiguousarray(srow, dtype=np.int32)
     crow = np.ascontiguousarray(crow, dtype=np.int32)
     sc = np.ascontiguousarray(scores, dtype=np.float64)
-    assert sc.shape == (srow.shape[0], K * a.V)
+    assert sc.shape == (srow.shape[0], head_columns(head))
     tokens = np.full((R, K), -1, dtype=np.int32)
     gap = np.full((R, K), np.inf)
     flags = np.zeros((R, K), dtype=np.uint32)

@@ -219,8 +219,21 @@ int32_t orc_sample_vector(const double *s, int32_t V, int32_t greedy, int32_t to
  * (Companion) row are partners through pair_map; solo audio rows and text
  * rows have no partner. */
 
+/* Size of stream k and the offset of its block in the N columns. */
+static int32_t orc_stream_V(const orc_step_args *a, int32_t k) {
+  return a->V_stream ? a->V_stream[k] : a->V;
+}
+
+static int64_t orc_stream_off(const orc_step_args *a, int32_t k) {
+  int64_t off = 0;
+  for (int32_t j = 0; j < k; ++j) off += orc_stream_V(a, j);
+  return off;
+}
+
 static int32_t orc_check_batch(const orc_step_args *a) {
   if (a->R < 0 || a->K <= 0 || a->V <= 0 || a->H <= 0) return ORC_E_SHAPE;
+  for (int32_t k = 0; k < a->K; ++k)
+    if (orc_stream_V(a, k) <= 0) return ORC_E_SHAPE;
   for (int32_t r = 0; r < a->R; ++r) {
     int32_t kind = a->row_kind[r], p = a->pair_map[r];
     if (kind == ORC_ROW_COND || kind == ORC_ROW_UNCOND) {
@@ -263,7 +276,7 @@ static void orc_emit_row(const orc_step_args *a, int32_t r, int32_t u, const dou
       token = a->pad_id;
       flags = ORC_FLAG_PAD;
     } else {
-      token = orc_sample_vector(s + (int64_t)k * a->V, a->V, greedy, a->top_k[r],
+      token = orc_sample_vector(s + orc_stream_off(a, k), orc_stream_V(a, k), greedy, a->top_k[r],
                                 (double)a->top_p[r], a->seed, key, t, k, a->gap_tol,
                                 a->topk_tol, a->topp_tol, &gap, &flags, NULL);
     }
@@ -280,7 +293,7 @@ static void orc_emit_row(const orc_step_args *a, int32_t r, int32_t u, const dou
 int32_t orc_head_step(const orc_step_args *a) {
   int32_t rc = orc_check_batch(a);
   if (rc != ORC_OK) return rc;
-  const int32_t N = a->K * a->V;
+  const int32_t N = (int32_t)orc_stream_off(a, a->K);
   double *lc = (double *)malloc(sizeof(double) * (size_t)N);
   double *lu = (double *)malloc(sizeof(double) * (size_t)N);
   double *sc = (double *)malloc(sizeof(double) * (size_t)N);
@@ -331,7 +344,7 @@ int32_t orc_head_step(const orc_step_args *a) {
 
 int32_t orc_sample_rows(const orc_step_args *a, int32_t Rs, const int32_t *srow,
                         const int32_t *crow, const double *scores) {
-  const int64_t N = (int64_t)a->K * a->V;
+  const int64_t N = orc_stream_off(a, a->K);
   for (int32_t i = 0; i < Rs; ++i) {
     int32_t r = srow[i];
     if (r < 0 || r >= a->R) return ORC_E_SHAPE;

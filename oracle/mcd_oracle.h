@@ -44,10 +44,15 @@ typedef struct {
   int32_t H, K, V, pad_id;
   const int32_t *delays;      /* [K] */
   int32_t dtype;              /* ORC_F32 or ORC_BF16: element type of hidden, W, W_text */
-  const void *W;              /* [K][V][H] */
-  const float *bias;          /* [K][V] or NULL */
+  const void *W;              /* [N][H]: [K][V][H] for equal streams */
+  const float *bias;          /* [N] or NULL */
   int32_t V_text;
   const void *W_text;         /* [V_text][H] or NULL */
+  /* Streams of unequal size (heterogeneous codebooks): stream k has V_stream[k]
+   * ids, its rows of W (and entries of bias, columns of scores) start at
+   * sum_{j<k} V_stream[j], and N = sum_k V_stream[k].  NULL: V for every
+   * stream, N = K * V. */
+  const int32_t *V_stream;    /* [K] or NULL */
   /* batch */
   int32_t R;
   const void *hidden;         /* [R][H] */
@@ -68,7 +73,7 @@ typedef struct {
   /* outputs (caller-allocated) */
   int32_t *tokens_out;        /* [R][K] */
   int32_t *frame_grid;        /* [n_slots][K][F_max]; only cells with a frame this step are written */
-  double *scores;             /* [R][K*V] or NULL: s for COND/SOLO rows, untouched otherwise */
+  double *scores;             /* [R][N] or NULL: s for COND/SOLO rows, untouched otherwise */
   double *gap;                /* [R][K] or NULL */
   uint32_t *flags;            /* [R][K] or NULL */
 } orc_step_args;
@@ -99,7 +104,7 @@ int32_t orc_sample_vector(const double *s, int32_t V, int32_t greedy, int32_t to
 int32_t orc_head_step(const orc_step_args *a);
 
 /* Sample a batch of ready-made scores (the part after the merge), rows given in
- * sampled order: scores[s][K*V], row s is physical row srow[s], companion crow[s]
+ * sampled order: scores[s][N], row s is physical row srow[s], companion crow[s]
  * (-1 for none).  Same outputs as orc_head_step for those rows. */
 int32_t orc_sample_rows(const orc_step_args *a, int32_t Rs, const int32_t *srow,
                         const int32_t *crow, const double *scores);

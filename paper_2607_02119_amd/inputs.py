@@ -8,8 +8,11 @@ arrays it returns.
 
 Recipe (fixed seeds; numpy's PCG64 via ``default_rng``):
   * stream-embedding term of the heads (when a workload asks for it): the fp32
-    bias b[k][v] = N(0,1) from default_rng([seed_w, 2000]), given as it is (the
-    product W_k e_k of a model's stream embedding e_k, precomputed).
+    bias b[n] = N(0,1) over the N columns from default_rng([seed_w, 2000]),
+    given as it is (the product W_k e_k of a model's stream embedding e_k,
+    precomputed).
+  * streams of unequal size (V_stream): stream k's V_stream[k] weight rows from
+    default_rng([seed_w, k]), all streams' rows stacked as W[N][H].
   * head weights  W_k = bf16_rne(N(0,1) / sqrt(H)) from default_rng([seed_w, k]),
     i.e. standard deviation 1/sqrt(H) so each logit is ~N(0,1); the text head
     W_text in 4096-row blocks b from default_rng([seed_w, 1000, b]).  fp32
@@ -66,6 +69,7 @@ class Workload:
     delays: tuple | None = None  # default d_k = k
     pad_id: int | None = None    # default V
     bias: bool = False           # stream-embedding term b[k][v] (W_k e_k) of the heads
+    V_stream: tuple | None = None  # ids per stream when they differ (V = the largest)
 
     @property
     def R(self) -> int:
@@ -73,7 +77,14 @@ class Workload:
 
     @property
     def N(self) -> int:
-        return self.K * self.V
+        return sum(self.stream_sizes)
+
+    @property
+    def stream_sizes(self) -> list:
+        if self.V_stream is None:
+            return [self.V] * self.K
+        assert len(self.V_stream) == self.K and max(self.V_stream) == self.V
+        return [int(v) for v in self.V_stream]
 
     @property
     def Rs(self) -> int:
@@ -148,9 +159,16 @@ def make_weights(wl: Workload, seed_w: int = SEED_W) -> dict:
     """Head weights: W[K][V][H] (uint16 bf16 bits or float32), W_text[V_text][H] or None."""
     scale = np.float32(1.0 / math.sqrt(wl.H))
     edt = np.uint16 if wl.dtype == "bf16" else np.float32
-    W = np.empty((wl.K, wl.V, wl.H), dtype=edt)
+    sizes = wl.stream_sizes
+    if wl.V_stream is None:
+        W = np.empty((wl.K, wl.V, wl.H), dtype=edt)
+        blocks = [W[k] for k in range(wl.K)]
+    else:                           # streams of unequal size: rows of all streams, [N][H]
+        W = np.empty((wl.N, wl.H), dtype=edt)
+        edges = np.concatenate([[0], np.cumsum(sizes)])
+        blocks = [W[edges[k]:edges[k + 1]] for k in range(wl.K)]
     for k in range(wl.K):
-        W[k] = _to_dtype(_normal([seed_w, k], (wl.V, wl.H)) * scale, wl.dtype)
+        blocks[k][...] = _to_dtype(_normal([seed_w, k], (sizes[k], wl.H)) * scale, wl.dtype)
     Wt = None
     if wl.n_text > 0 or wl.V_text > 0:
         Wt = np.empty((wl.V_text, wl.H), dtype=edt)
@@ -161,9 +179,14 @@ def make_weights(wl: Workload, seed_w: int = SEED_W) -> dict:
                                        wl.dtype)
     bias = None
     if wl.bias:
-        bias = np.ascontiguousarray(_normal([seed_w, 2000], (wl.K, wl.V)))
-    return dict(H=wl.H, K=wl.K, V=wl.V, pad_id=wl.pad, delays=np.array(wl.delay_list, np.int32),
+        bias = np.ascontiguousarray(_normal([seed_w, 2000], (wl.N,)))
+        if wl.V_stream is None:
+            bias = bias.reshape(wl.K, wl.V)
+    head = dict(H=wl.H, K=wl.K, V=wl.V, pad_id=wl.pad, delays=np.array(wl.delay_list, np.int32),
                 W=W, bias=bias, W_text=Wt)
+    if wl.V_stream is not None:
+        head["V_stream"] = np.array(sizes, np.int32)
+    return head
 
 
 def make_embeddings(wl: Workload, seed_e: int = SEED_E) -> dict:

@@ -42,16 +42,20 @@ def pick_rows(layout: dict, n_pairs=2, n_solo=2, n_text=2, seed=0):
     return sorted(out)
 
 
-def score_rel_err(gpu_scores, plan_rows, ora_scores, K, V):
-    """max over (row, k) vectors of max|g - o| / max|o|; plan_rows[s] = physical row."""
+def score_rel_err(gpu_scores, plan_rows, ora_scores, sizes):
+    """max over (row, k) vectors of max|g - o| / max|o|; plan_rows[s] = physical row;
+    sizes[k] = ids of stream k (the vectors' lengths, in column order)."""
     worst = 0.0
+    edges = np.concatenate([[0], np.cumsum(sizes)])
     for s, r in enumerate(plan_rows):
         if r is None:
             continue
-        g = gpu_scores[s].astype(np.float64).reshape(K, V)
-        o = ora_scores[r].reshape(K, V)
-        den = np.maximum(np.abs(o).max(axis=1), 1e-300)
-        worst = max(worst, float((np.abs(g - o).max(axis=1) / den).max()))
+        g = gpu_scores[s].astype(np.float64)
+        o = ora_scores[r]
+        for k in range(len(sizes)):
+            gk, ok = g[edges[k]:edges[k + 1]], o[edges[k]:edges[k + 1]]
+            den = max(float(np.abs(ok).max()), 1e-300)
+            worst = max(worst, float(np.abs(gk - ok).max()) / den)
     return worst
 
 

@@ -62,7 +62,7 @@ def _check_step(dw, t, tc, rows=None, score_tol=None):
     tc.add(g_tok[sel], o["tokens"], o["flags"], where=f"t={t}")
     if score_tol is not None and dw.wl.Rs:
         err = score_rel_err(g_sc, _plan_rows(dw, None if rows is None else list(sel)), o["scores"],
-                            dw.wl.K, dw.wl.V)
+                            oracle.stream_sizes(dw.host_head))
         say(f"  t={t} score rel err {err:.3e}")
         assert err <= score_tol
     return g_tok, o

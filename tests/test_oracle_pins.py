@@ -559,3 +559,53 @@ def test_next_input_rejects_bad_tokens():
     with pytest.raises(ValueError):                          # text id past the text table
         oracle.next_input(E, np.array([[5, 0]], np.int32), np.array([3], np.uint8), pad_id=9,
                           E_text=np.zeros((5, 2), np.float32))
+
+
+# ---------------------------------------------------------------------------
+# Streams of unequal size (heterogeneous codebooks): stream k has V_k ids.
+
+@pytest.mark.parametrize("sampling", [dict(top_k=5), dict(top_p=0.8), dict(temperature=0.0),
+                                      dict(top_k=9, top_p=0.9)])
+def test_unequal_streams_equal_masked_equal_streams(sampling):
+    """A head whose stream k has V_k ids gives the tokens and scores of an
+    equal-stream head of V ids whose ids past V_k in stream k carry a bias of
+    -1e30 (they can never be kept or drawn).  Both run through the oracle's
+    whole step; only the offsets of the unequal form differ."""
+    sizes = (11, 4, 7)
+    K, V = len(sizes), max(sizes)
+    wl = inputs.Workload("u", H=32, K=K, V=V, n_pairs=2, n_solo=2, dtype="f32", steps=6,
+                         shuffle=True, **sampling)
+    head = inputs.make_weights(wl)
+    lay = inputs.row_layout(wl)
+    bias = np.zeros((K, V), np.float32)
+    for k, vk in enumerate(sizes):
+        bias[k, vk:] = -1e30
+    head_eq = dict(head, bias=bias)
+    head_un = dict(head, V_stream=np.array(sizes, np.int32),
+                   W=np.concatenate([head["W"][k, :vk] for k, vk in enumerate(sizes)]),
+                   bias=np.zeros(sum(sizes), np.float32))
+    edges = np.concatenate([[0], np.cumsum(sizes)])
+    n_drawn = 0
+    for t in range(wl.steps):
+        b = inputs.make_batch(wl, t, lay)
+        eq = oracle.head_step(head_eq, b)
+        un = oracle.head_step(head_un, b)
+        assert np.array_equal(eq["tokens"], un["tokens"]), t
+        for k, vk in enumerate(sizes):
+            cols = eq["scores"][:, k * V:k * V + vk]
+            live = ~np.isnan(cols[:, 0])
+            assert np.array_equal(cols[live], un["scores"][:, edges[k]:edges[k + 1]][live])
+            tok = un["tokens"][:, k]
+            assert ((tok == wl.pad) | ((tok >= 0) & (tok < vk))).all()
+            n_drawn += int(((tok >= 0) & (tok < vk)).sum())
+    assert n_drawn > 0
+
+
+def test_unequal_streams_all_equal_is_the_equal_stream_head():
+    wl, head, lay = _tiny(n_pairs=2, n_solo=1, K=3, V=13, steps=5, top_k=4, shuffle=True)
+    head_un = dict(head, V_stream=np.full(3, 13, np.int32), W=head["W"].reshape(39, wl.H))
+    for t in range(wl.steps):
+        b = inputs.make_batch(wl, t, lay)
+        a, u = oracle.head_step(head, b), oracle.head_step(head_un, b)
+        assert np.array_equal(a["tokens"], u["tokens"])
+        assert np.array_equal(a["scores"], u["scores"], equal_nan=True)
