@@ -74,18 +74,27 @@ enum {
 typedef struct mcd_head mcd_head;   /* opaque, immutable after creation, thread-safe */
 
 /* Head description.  The weights are borrowed: they must stay valid and
- * unchanged while the handle is used. */
+ * unchanged while the handle is used.
+ *
+ * Streams of unequal size (heterogeneous codebooks, e.g. one SSL stream and
+ * eight codec streams): V_stream[k] ids for stream k, V the largest of them.
+ * Stream k's block of the N = sum_k V_stream[k] columns starts at
+ * off_k = sum_{j<k} V_stream[j]: rows off_k + v of W and entries of bias, and
+ * the same columns of every scores row.  With V_stream NULL every stream has
+ * V ids, off_k = k*V and N = K*V. */
 typedef struct {
   int32_t H;                 /* hidden size; multiple of 64 for MCD_BF16, of 4 for MCD_F32 */
   int32_t K;                 /* codebooks (streams), 1..MCD_MAX_K */
-  int32_t V;                 /* audio sub-vocabulary per codebook, 1..MCD_MAX_V */
+  int32_t V;                 /* audio sub-vocabulary per codebook (the largest), 1..MCD_MAX_V */
   int32_t pad_id;            /* token emitted where the delay pattern has no frame */
   const int32_t *delays;     /* [host][K] d_k >= 0; copied at creation */
   mcd_dtype dtype;           /* element type of hidden, W and W_text */
-  const void *W;             /* [K][V][H]: row n = k*V + v is head k's weight for id v */
-  const float *bias;         /* [K][V] or NULL: stream-embedding term W_k e_k */
+  const void *W;             /* [N][H]: row off_k + v is head k's weight for id v */
+  const float *bias;         /* [N] or NULL: stream-embedding term W_k e_k */
   int32_t V_text;            /* text vocabulary of the text head, 0 if none */
   const void *W_text;        /* [V_text][H] or NULL */
+  const int32_t *V_stream;   /* [host][K] ids of each stream (1..MCD_MAX_V), or NULL;
+                                copied at creation */
 } mcd_head_desc;
 
 mcd_status mcd_head_create(const mcd_head_desc *desc, mcd_head **out);
@@ -139,7 +148,7 @@ typedef struct {
                                 TEXT: [r][0] greedy text id, the rest pad_id */
   int32_t *frame_grid;       /* [n_slots][K][F_max] or NULL; cell [slot][k][t - d_k] written */
   int32_t n_slots, F_max;
-  float *scores;             /* [n_pairs + n_solo][K*V] fp32 in sampled order: the merged,
+  float *scores;             /* [n_pairs + n_solo][N] fp32 in sampled order: the merged,
                                 temperature-divided logits (greedy rows: merged only).
                                 Output of mcd_head_step, input of mcd_sample_step. */
   void *workspace;

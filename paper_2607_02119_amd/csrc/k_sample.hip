@@ -1152,10 +1152,12 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
   // The scores depend only on the vector index: their loads go out first.
   float x[EPL];
   uint32_t active = 0;
-  const int V = hv.V;
+  // stream k's block of the score row: V ids from column off
+  const int off = hv.voff.o[k];
+  const int V = hv.voff.o[k + 1] - off;
   if (audio) {
-    const float *sc = sv.scores + (size_t)s * hv.N + (size_t)k * V;
-    if ((V & 3) == 0) {
+    const float *sc = sv.scores + (size_t)s * hv.N + off;
+    if (((V | off | hv.N) & 3) == 0) {   // 16-byte aligned whole groups
 #pragma unroll
       for (int q = 0; q < GPT; ++q) {
         const int g = q * TPV + gt;

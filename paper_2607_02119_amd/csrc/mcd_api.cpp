@@ -181,12 +181,24 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
   mcd::Delays del;
   int32_t max_d;
   if (!make_delays(d->delays, d->K, del, max_d)) return fail(MCD_E_INVALID, "bad delays");
+  // stream blocks: V ids each, or V_stream[k] ids with V the largest
+  mcd::StreamOffsets voff;
+  voff.o[0] = 0;
+  int32_t vmax = 0;
+  for (int32_t k = 0; k < d->K; ++k) {
+    const int32_t vk = d->V_stream ? d->V_stream[k] : d->V;
+    if (vk < 1 || vk > MCD_MAX_V)
+      return fail(MCD_E_UNSUPPORTED, "stream %d: %d ids, outside 1..%d", k, vk, MCD_MAX_V);
+    voff.o[k + 1] = voff.o[k] + vk;
+    vmax = vk > vmax ? vk : vmax;
+  }
+  if (vmax != d->V) return fail(MCD_E_INVALID, "V=%d is not the largest stream (%d)", d->V, vmax);
   mcd_head *h = new (std::nothrow) mcd_head;
   if (!h) return fail(MCD_E_INVALID, "out of host memory");
   h->hv.H = d->H;
   h->hv.K = d->K;
   h->hv.V = d->V;
-  h->hv.N = d->K * d->V;
+  h->hv.N = voff.o[d->K];
   h->hv.pad_id = d->pad_id;
   h->hv.V_text = d->V_text;
   h->hv.dtype = d->dtype;
@@ -194,6 +206,7 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
   h->hv.bias = d->bias;
   h->hv.W_text = d->V_text > 0 ? d->W_text : nullptr;
   h->hv.delays = del;
+  h->hv.voff = voff;
   h->max_delay = max_d;
   *out = h;
   return MCD_OK;

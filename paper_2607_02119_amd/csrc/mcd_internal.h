@@ -24,7 +24,12 @@ struct Delays {
   int32_t d[MCD_MAX_K];
 };
 
-// Head, by value in kernel arguments.
+// First column of every stream's block in the N columns; voff[K] = N.
+struct StreamOffsets {
+  int32_t o[MCD_MAX_K + 1];
+};
+
+// Head, by value in kernel arguments.  V is the largest stream's size.
 struct HeadView {
   int32_t H, K, V, N, pad_id, V_text;
   int32_t dtype;
@@ -32,6 +37,7 @@ struct HeadView {
   const float *bias;
   const void *W_text;
   Delays delays;
+  StreamOffsets voff;
 };
 
 // One step, by value in kernel arguments.

@@ -38,10 +38,11 @@ class DeviceWorkload:
         W = to_device(hh["W"], device)
         Wt = None if hh["W_text"] is None else to_device(hh["W_text"], device)
         b = None if hh.get("bias") is None else to_device(hh["bias"], device)
-        self.heads = [mcd.Head(W, hh["delays"], hh["pad_id"], b, Wt)]
+        vs = hh.get("V_stream")
+        self.heads = [mcd.Head(W, hh["delays"], hh["pad_id"], b, Wt, vs)]
         for _ in range(1, weight_copies):
             self.heads.append(mcd.Head(W.clone(), hh["delays"], hh["pad_id"], b,
-                                       None if Wt is None else Wt.clone()))
+                                       None if Wt is None else Wt.clone(), vs))
         self.plan = self.heads[0].plan(self.layout["pair_map"], self.layout["row_kind"], device)
         R, K = wl.R, wl.K
         b0 = inputs.make_batch(wl, 0, self.layout)

@@ -34,7 +34,7 @@ _i32 = ctypes.c_int32
 class mcd_head_desc(ctypes.Structure):
     _fields_ = [("H", _i32), ("K", _i32), ("V", _i32), ("pad_id", _i32),
                 ("delays", _vp), ("dtype", ctypes.c_int), ("W", _vp), ("bias", _vp),
-                ("V_text", _i32), ("W_text", _vp)]
+                ("V_text", _i32), ("W_text", _vp), ("V_stream", _vp)]
 
 
 class mcd_batch_counts(ctypes.Structure):
@@ -130,10 +130,12 @@ def mcd_last_error():
     return _mcd_last_error().decode(errors="replace")
 
 
-def mcd_head_create(H, K, V, pad_id, delays, dtype, W, bias=None, V_text=0, W_text=None):
+def mcd_head_create(H, K, V, pad_id, delays, dtype, W, bias=None, V_text=0, W_text=None,
+                    V_stream=None):
     d = np.ascontiguousarray(delays, dtype=np.int32)
+    vs = None if V_stream is None else np.ascontiguousarray(V_stream, dtype=np.int32)
     desc = mcd_head_desc(H, K, V, pad_id, d.ctypes.data, dtype, _ptr(W), _ptr(bias), V_text,
-                         _ptr(W_text))
+                         _ptr(W_text), _ptr(vs))
     h = _vp()
     _check(_mcd_head_create(ctypes.byref(desc), ctypes.byref(h)), "mcd_head_create")
     return h
@@ -236,16 +238,23 @@ def mcd_read_device_status(workspace, stream=None):
 class Head:
     """Handle plus the device tensors it borrows."""
 
-    def __init__(self, W, delays, pad_id, bias=None, W_text=None):
-        assert W.is_cuda and W.dim() == 3 and W.is_contiguous()
-        K, V, H = W.shape
+    def __init__(self, W, delays, pad_id, bias=None, W_text=None, V_stream=None):
+        """W: [K][V][H], or [N][H] with V_stream (the ids of each stream)."""
+        assert W.is_cuda and W.is_contiguous()
+        if V_stream is None:
+            assert W.dim() == 3
+            K, V, H = W.shape
+        else:
+            V_stream = np.ascontiguousarray(V_stream, dtype=np.int32)
+            assert W.dim() == 2 and W.shape[0] == int(V_stream.sum())
+            K, V, H = V_stream.shape[0], int(V_stream.max()), W.shape[1]
         dtype = {torch.bfloat16: MCD_BF16, torch.float32: MCD_F32}[W.dtype]
-        self.W, self.bias, self.W_text = W, bias, W_text
+        self.W, self.bias, self.W_text, self.V_stream = W, bias, W_text, V_stream
         self.H, self.K, self.V, self.pad_id = H, K, V, int(pad_id)
         self.delays = np.ascontiguousarray(delays, dtype=np.int32)
         self.V_text = 0 if W_text is None else W_text.shape[0]
         self.handle = mcd_head_create(H, K, V, self.pad_id, self.delays, dtype, W, bias,
-                                      self.V_text, W_text)
+                                      self.V_text, W_text, V_stream)
 
     def __del__(self):
         h = getattr(self, "handle", None)

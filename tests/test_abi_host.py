@@ -49,6 +49,12 @@ def test_head_create_validation():
             _head(**b)
     h = _head(dtype=mcd.MCD_F32, H=40)
     mcd.mcd_head_destroy(h)
+    # streams of unequal size: V is the largest, every stream 1..MCD_MAX_V ids
+    h = _head(V_stream=[50, 7, 13])
+    mcd.mcd_head_destroy(h)
+    for vs in ([50, 0, 3], [10, 20, 30], [50, 51, 3], [mcd.MCD_MAX_V + 1, 1, 1]):
+        with pytest.raises(mcd.McdError):
+            _head(V_stream=vs, V=50)
 
 
 def test_batch_plan_layout_and_errors():

@@ -122,6 +122,20 @@ RAGGED = [
     # 128-row 256-column tiles, fewer slices than weight stages (H = 192)
     ("stream_wide_bm128", dict(H=192, K=9, V=3700, n_pairs=60, n_solo=5, n_text=100,
                                V_text=40000, dtype="bf16", top_p=0.9, cfg_w=2.5, steps=10)),
+    # streams of unequal size (one large stream and smaller ones): the
+    # streaming kernel with N % 4 != 0, the 256 x 128 MFMA kernel, and the
+    # one-wave-per-vector sampler
+    ("unequal_streams_stream", dict(H=128, K=4, V=100, V_stream=(100, 37, 64, 5), n_pairs=6,
+                                    n_solo=2, n_text=2, V_text=300, dtype="bf16", top_k=7,
+                                    temperature=0.8, steps=6, shuffle=True, bias=True)),
+    ("unequal_streams_mfma", dict(H=64, K=9, V=2048, V_stream=(2048,) + (1024,) * 8,
+                                  n_pairs=100, n_solo=60, dtype="bf16", top_p=0.9, cfg_w=2.5,
+                                  steps=10)),
+    ("unequal_streams_wave", dict(H=64, K=8, V=1000, V_stream=(1000, 500, 250, 125, 1000, 999, 3, 64),
+                                  n_pairs=64, n_solo=80, dtype="bf16", top_k=20, steps=8,
+                                  shuffle=True)),
+    ("unequal_streams_f32", dict(H=40, K=3, V=37, V_stream=(37, 2, 20), n_pairs=3, n_solo=2,
+                                 n_text=1, V_text=70, dtype="f32", top_p=0.8, steps=5)),
     # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
     ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
                                 temperature=0.9, steps=4, shuffle=True)),
