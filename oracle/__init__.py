@@ -93,7 +93,7 @@ class StepArgs(ctypes.Structure):
         ("delays", ctypes.c_void_p), ("dtype", ctypes.c_int32),
         ("W", ctypes.c_void_p), ("bias", ctypes.c_void_p),
         ("V_text", ctypes.c_int32), ("W_text", ctypes.c_void_p),
-        ("V_stream", ctypes.c_void_p),
+        ("V_stream", ctypes.c_void_p), ("T_text", ctypes.c_int32),
         ("R", ctypes.c_int32), ("hidden", ctypes.c_void_p),
         ("pair_map", ctypes.c_void_p), ("row_kind", ctypes.c_void_p),
         ("cfg_w", ctypes.c_void_p), ("temperature", ctypes.c_void_p),
@@ -104,6 +104,7 @@ class StepArgs(ctypes.Structure):
         ("gap_tol", ctypes.c_double), ("topk_tol", ctypes.c_double),
         ("topp_tol", ctypes.c_double),
         ("tokens_out", ctypes.c_void_p), ("frame_grid", ctypes.c_void_p),
+        ("modality", ctypes.c_void_p), ("modality_gap", ctypes.c_void_p),
         ("scores", ctypes.c_void_p), ("gap", ctypes.c_void_p), ("flags", ctypes.c_void_p),
     ]
 
@@ -231,6 +232,7 @@ def _step_struct(head, batch, seed, n_slots, F_max, tol, keep):
     arrs["rng_key"] = _c(rk, np.uint64)
     keep += [W, delays, bias, Wt, hidden, vs] + list(arrs.values())
     a.V_stream = _ptr(vs)
+    a.T_text = int(head.get("T_text") or 0)
     a.H, a.K, a.V, a.pad_id = H, K, V, head["pad_id"]
     a.delays, a.dtype, a.W, a.bias = delays.ctypes.data, dtype, W.ctypes.data, _ptr(bias)
     a.V_text = 0 if Wt is None else Wt.shape[0]
@@ -264,7 +266,8 @@ def head_step(head, batch, seed=0, n_slots=0, F_max=0, frame_grid=None,
     batch: dict(hidden[R][H], pair_map, row_kind, cfg_w, temperature, top_k, top_p,
                 rng_key or None, step, n_frames, grid_slot)
     Returns dict(tokens[R][K], scores[R][N] (fp64, COND/SOLO rows), gap[R][K], flags[R][K],
-                 frame_grid) -- frame_grid is updated in place when given.
+                 frame_grid, modality[R], modality_gap[R]) -- frame_grid is updated in place
+    when given; modality (TEXT rows) follows head["T_text"], the text ids of the text head.
     """
     keep = []
     a = _step_struct(head, batch, seed, n_slots, F_max, (gap_tol, topk_tol, topp_tol), keep)
@@ -277,12 +280,16 @@ def head_step(head, batch, seed=0, n_slots=0, F_max=0, frame_grid=None,
     if frame_grid is not None:
         assert frame_grid.dtype == np.int32 and frame_grid.flags.c_contiguous
         assert frame_grid.shape == (n_slots, K, F_max)
+    modality = np.zeros(R, dtype=np.uint8)
+    modality_gap = np.full(R, np.inf)
     a.tokens_out, a.frame_grid = tokens.ctypes.data, _ptr(frame_grid)
+    a.modality, a.modality_gap = modality.ctypes.data, modality_gap.ctypes.data
     a.scores, a.gap, a.flags = _ptr(scores), gap.ctypes.data, flags.ctypes.data
     rc = lib().orc_head_step(ctypes.byref(a))
     if rc:
         raise ValueError("oracle head_step: " + ERRORS.get(rc, str(rc)))
-    return dict(tokens=tokens, scores=scores, gap=gap, flags=flags, frame_grid=frame_grid)
+    return dict(tokens=tokens, scores=scores, gap=gap, flags=flags, frame_grid=frame_grid,
+                modality=modality, modality_gap=modality_gap)
 
 
 def sample_rows(head, batch, srow, crow, scores, seed=0, n_slots=0, F_max=0, frame_grid=None,
@@ -333,3 +340,43 @@ def next_input(E, tokens, row_kind, pad_id, E_text=None):
     if rc:
         raise ValueError(ERRORS.get(rc, rc))
     return out
+
+
+# --------------------------------------------------------------------------
+# Mixed-modality phase of a request (Sec. 2.2)
+
+PHASE_TEXT, PHASE_BRIDGE, PHASE_AUDIO, PHASE_DRAIN = 0, 1, 2, 3
+
+
+def phase_advance(phase, count, token0, modality, bridge, audio_end, drain_steps):
+    """One decode step of one request's phase -> (phase, count, emit).
+
+    TEXT: the request's row emitted token0, its greedy token over the text
+      ids (the vocabulary mask).  When the unmasked argmax lay outside the
+      text ids (modality = 1) the request leaves the text phase: it emits the
+      first bridging token instead and continues with the rest of them, or,
+      with no bridging tokens, keeps token0 and goes straight to AUDIO.
+    BRIDGE: emits bridge[count]; after the last one, AUDIO.
+    AUDIO: the head's sampled tokens are the output (emit -1); a stream-0
+      token equal to audio_end ends the phase.
+    DRAIN: drain_steps steps (the largest delay, S - 1) in which the delayed
+      streams finish their frames and the rest are pads (emit -1); then TEXT.
+    count: bridging tokens emitted (BRIDGE), audio steps taken (AUDIO),
+    drain steps taken (DRAIN)."""
+    nb = len(bridge)
+    if phase == PHASE_TEXT:
+        if not modality:
+            return PHASE_TEXT, 0, token0
+        if nb == 0:
+            return PHASE_AUDIO, 0, token0
+        return (PHASE_BRIDGE, 1, bridge[0]) if nb > 1 else (PHASE_AUDIO, 0, bridge[0])
+    if phase == PHASE_BRIDGE:
+        emit = bridge[count]
+        return (PHASE_AUDIO, 0, emit) if count + 1 >= nb else (PHASE_BRIDGE, count + 1, emit)
+    if phase == PHASE_AUDIO:
+        if token0 == audio_end:
+            return (PHASE_DRAIN, 0, -1) if drain_steps > 0 else (PHASE_TEXT, 0, -1)
+        return PHASE_AUDIO, count + 1, -1
+    if phase == PHASE_DRAIN:
+        return (PHASE_TEXT, 0, -1) if count + 1 >= drain_steps else (PHASE_DRAIN, count + 1, -1)
+    raise ValueError(f"unknown phase {phase}")

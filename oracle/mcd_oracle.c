@@ -306,8 +306,21 @@ int32_t orc_head_step(const orc_step_args *a) {
       orc_logits_row(hrow, a->dtype, a->W_text, NULL, a->H, a->V_text, lt);
       double gap = INFINITY;
       uint32_t flags = 0;
-      int32_t tok = orc_sample_vector(lt, a->V_text, 1, 0, 1.0, a->seed, 0, 0, 0,
+      /* vocabulary mask of the text phase: the token is the greedy one over
+       * the text ids; the modality is where the unmasked argmax lies */
+      int32_t T = (a->T_text > 0 && a->T_text < a->V_text) ? a->T_text : a->V_text;
+      int32_t tok = orc_sample_vector(lt, T, 1, 0, 1.0, a->seed, 0, 0, 0,
                                       a->gap_tol, a->topk_tol, a->topp_tol, &gap, &flags, NULL);
+      int32_t best = 0;
+      for (int32_t v = 1; v < a->V_text; ++v)
+        if (lt[v] > lt[best]) best = v;      /* strict: the lowest id on ties */
+      double mt = -INFINITY, mo = -INFINITY;
+      for (int32_t v = 0; v < a->V_text; ++v) {
+        if (v < T) mt = lt[v] > mt ? lt[v] : mt;
+        else mo = lt[v] > mo ? lt[v] : mo;
+      }
+      if (a->modality) a->modality[r] = (uint8_t)(best >= T);
+      if (a->modality_gap) a->modality_gap[r] = T < a->V_text ? fabs(mt - mo) : INFINITY;
       for (int32_t k = 0; k < a->K; ++k) {
         a->tokens_out[(int64_t)r * a->K + k] = (k == 0) ? tok : a->pad_id;
         if (a->gap) a->gap[(int64_t)r * a->K + k] = (k == 0) ? gap : INFINITY;

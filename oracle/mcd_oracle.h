@@ -53,6 +53,12 @@ typedef struct {
    * sum_{j<k} V_stream[j], and N = sum_k V_stream[k].  NULL: V for every
    * stream, N = K * V. */
   const int32_t *V_stream;    /* [K] or NULL */
+  /* Text-phase vocabulary mask (Sec. 2.2): ids [0, T_text) of the text head
+   * are text tokens, the rest belong to other modalities.  A TEXT row emits
+   * the greedy token over the text ids only; its modality is read from the
+   * unmasked distribution: 1 when the argmax over all V_text ids (lowest id
+   * on ties) lies outside the text ids.  0 or V_text: no mask. */
+  int32_t T_text;
   /* batch */
   int32_t R;
   const void *hidden;         /* [R][H] */
@@ -73,6 +79,8 @@ typedef struct {
   /* outputs (caller-allocated) */
   int32_t *tokens_out;        /* [R][K] */
   int32_t *frame_grid;        /* [n_slots][K][F_max]; only cells with a frame this step are written */
+  uint8_t *modality;          /* [R] or NULL: TEXT rows' modality flag, untouched otherwise */
+  double *modality_gap;       /* [R] or NULL: |max over text ids - max over the rest| */
   double *scores;             /* [R][N] or NULL: s for COND/SOLO rows, untouched otherwise */
   double *gap;                /* [R][K] or NULL */
   uint32_t *flags;            /* [R][K] or NULL */

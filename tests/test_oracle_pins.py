@@ -609,3 +609,67 @@ def test_unequal_streams_all_equal_is_the_equal_stream_head():
         a, u = oracle.head_step(head, b), oracle.head_step(head_un, b)
         assert np.array_equal(a["tokens"], u["tokens"])
         assert np.array_equal(a["scores"], u["scores"], equal_nan=True)
+
+
+# ---------------------------------------------------------------------------
+# Mixed-modality phases (Sec. 2.2): the text phase's vocabulary mask, modality
+# inference from the unmasked distribution, and the phase state machine.
+
+def test_text_mask_and_modality_against_numpy_argmax():
+    """TEXT rows: the token is the argmax over the text ids [0, T) and the
+    modality flag says whether the argmax over all ids lies past them; both
+    checked against numpy's fp64 matmul and argmax (lowest id on ties)."""
+    wl, head, lay = _tiny(n_pairs=1, n_solo=1, n_text=6, K=2, V=11, steps=3, top_k=3)
+    T = 32
+    head = dict(head, T_text=T)
+    Wt = head["W_text"].astype(np.float64)
+    # make rows of the non-text region win for some rows: scale it up
+    Wt2 = head["W_text"].copy()
+    Wt2[T:] *= 3.0
+    head2 = dict(head, W_text=Wt2)
+    seen = set()
+    for hd, W in ((head, Wt), (head2, Wt2.astype(np.float64))):
+        for t in range(wl.steps):
+            b = inputs.make_batch(wl, t, lay)
+            out = oracle.head_step(hd, b)
+            for r in np.flatnonzero(lay["row_kind"] == inputs.ROW_TEXT):
+                lt = W @ b["hidden"][r].astype(np.float64)
+                assert out["tokens"][r, 0] == int(np.argmax(lt[:T]))
+                assert out["modality"][r] == int(int(np.argmax(lt)) >= T)
+                seen.add(int(out["modality"][r]))
+    assert seen == {0, 1}
+
+
+def test_no_text_mask_keeps_the_plain_greedy_text_token():
+    wl, head, lay = _tiny(n_pairs=1, n_solo=1, n_text=3, K=2, V=11, steps=2, top_k=3)
+    for T in (0, wl.V_text):
+        for t in range(wl.steps):
+            b = inputs.make_batch(wl, t, lay)
+            a, m = oracle.head_step(head, b), oracle.head_step(dict(head, T_text=T), b)
+            assert np.array_equal(a["tokens"], m["tokens"])
+            assert (m["modality"] == 0).all()
+
+
+def test_phase_machine_hand_traced():
+    P = oracle
+    bridge, end, drain = [900, 901], 7, 2
+    seq = [  # (phase, count, token0, modality) -> (phase, count, emit)
+        ((P.PHASE_TEXT, 0, 5, 0), (P.PHASE_TEXT, 0, 5)),
+        ((P.PHASE_TEXT, 0, 6, 1), (P.PHASE_BRIDGE, 1, 900)),
+        ((P.PHASE_BRIDGE, 1, 0, 0), (P.PHASE_AUDIO, 0, 901)),
+        ((P.PHASE_AUDIO, 0, 3, 0), (P.PHASE_AUDIO, 1, -1)),
+        ((P.PHASE_AUDIO, 1, 7, 0), (P.PHASE_DRAIN, 0, -1)),
+        ((P.PHASE_DRAIN, 0, 0, 0), (P.PHASE_DRAIN, 1, -1)),
+        ((P.PHASE_DRAIN, 1, 0, 0), (P.PHASE_TEXT, 0, -1)),
+        ((P.PHASE_TEXT, 0, 8, 0), (P.PHASE_TEXT, 0, 8)),
+    ]
+    state = (P.PHASE_TEXT, 0)
+    for (ph, c, tok, mod), want in seq:
+        assert state == (ph, c)
+        got = P.phase_advance(ph, c, tok, mod, bridge, end, drain)
+        assert got == want
+        state = got[:2]
+    # no bridging tokens: straight to audio, keeping the text token; no drain
+    assert P.phase_advance(P.PHASE_TEXT, 0, 6, 1, [], end, 0) == (P.PHASE_AUDIO, 0, 6)
+    assert P.phase_advance(P.PHASE_AUDIO, 4, 7, 0, [], end, 0) == (P.PHASE_TEXT, 0, -1)
+    assert P.phase_advance(P.PHASE_TEXT, 0, 6, 1, [42], end, 0) == (P.PHASE_AUDIO, 0, 42)
