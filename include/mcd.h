@@ -95,6 +95,9 @@ typedef struct {
   const void *W_text;        /* [V_text][H] or NULL */
   const int32_t *V_stream;   /* [host][K] ids of each stream (1..MCD_MAX_V), or NULL;
                                 copied at creation */
+  int32_t T_text;            /* text-phase vocabulary mask (Sec. 2.2): ids [0, T_text) of the
+                                text head are text tokens, the rest mark other modalities.
+                                0 or V_text: no mask; else a multiple of 32 below V_text */
 } mcd_head_desc;
 
 mcd_status mcd_head_create(const mcd_head_desc *desc, mcd_head **out);
@@ -147,6 +150,9 @@ typedef struct {
   int32_t *tokens_out;       /* [R][K]: COND/SOLO sampled, UNCOND = its Main row's,
                                 TEXT: [r][0] greedy text id, the rest pad_id */
   int32_t *frame_grid;       /* [n_slots][K][F_max] or NULL; cell [slot][k][t - d_k] written */
+  uint8_t *modality_out;     /* [R] or NULL: for TEXT rows, 1 when the argmax over all text-head
+                                ids lies outside [0, T_text) (the model asks to leave the
+                                text phase), else 0; other rows untouched */
   int32_t n_slots, F_max;
   float *scores;             /* [n_pairs + n_solo][N] fp32 in sampled order: the merged,
                                 temperature-divided logits (greedy rows: merged only).
@@ -189,6 +195,43 @@ mcd_status mcd_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, in
 mcd_status mcd_interleave(const int32_t *grid, int32_t n_req, int32_t F, int32_t K,
                           const int32_t *delays /*[host][K]*/, int32_t pad_id,
                           int32_t *streams, hipStream_t stream);
+
+/* ---- mixed-modality phases (Sec. 2.2) -------------------------------------
+ * Each request moves through a text phase (TEXT rows: greedy over the text
+ * ids, the mask of mcd_head_desc.T_text), a transition that injects
+ * deterministic bridging tokens, an audio phase (audio rows: all K streams),
+ * and a drain of S - 1 steps that flushes the delayed streams, then back to
+ * text.  The switch out of text is read from the unmasked distribution
+ * (mcd_step_args.modality_out).  The caller re-plans its batch when a
+ * request's row kind changes (TEXT rows in the text phase, audio rows in the
+ * audio and drain phases; the drain ends the request's frames through
+ * n_frames). */
+enum { MCD_PHASE_TEXT = 0, MCD_PHASE_BRIDGE = 1, MCD_PHASE_AUDIO = 2, MCD_PHASE_DRAIN = 3 };
+
+typedef struct {
+  int32_t n_bridge;          /* bridging tokens between text and audio, >= 0 */
+  const int32_t *bridge;     /* [host][n_bridge] their ids */
+  int32_t audio_end;         /* stream-0 token that ends the audio phase */
+  int32_t drain_steps;       /* steps of the drain: the largest delay (S - 1), >= 0 */
+} mcd_phase_desc;
+
+/* [host] One decode step of n requests' phases, in place.  For request i:
+ * phase[i], count[i] (bridging tokens emitted / audio steps / drain steps);
+ * token0[i]: its stream-0 token of this step (the masked text token of a
+ * text-phase row); modality[i]: its modality flag (text phase only).  emit[i]
+ * receives the token the request emits this step outside the head's audio
+ * output (text token or bridging token), or -1.
+ *   TEXT:   modality 0 -> stay, emit token0; modality 1 -> emit bridge[0] and
+ *           go to BRIDGE (AUDIO if that was the only one; with none, emit
+ *           token0 and go to AUDIO).
+ *   BRIDGE: emit bridge[count]; after the last, AUDIO.
+ *   AUDIO:  token0 == audio_end -> DRAIN (TEXT if drain_steps is 0).
+ *   DRAIN:  after drain_steps steps, TEXT.
+ * MCD_E_INVALID for bad sizes, an unknown phase or a count out of range (the
+ * arrays are then unchanged from that request on). */
+mcd_status mcd_phase_advance(const mcd_phase_desc *desc, int32_t n, uint8_t *phase,
+                             int32_t *count, const int32_t *token0, const uint8_t *modality,
+                             int32_t *emit);
 
 /* ---- next-step input (Sec. 2.1, delay pattern) ----------------------------
  * The backbone's input for the next step aggregates the embeddings of the K

@@ -1210,16 +1210,27 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     return;
   }
   if (!audio) {
-    // text row: reduce the (max, lowest argmax) partials of the text GEMM
+    // text row: reduce the (max, lowest argmax) partials of the text GEMM.
+    // The text phase's mask (Sec. 2.2): the token is the best over the text
+    // ids [0, T_text), whole 32-column parts; the modality is where the best
+    // over all ids lies (text ids are the lower ones, so ties stay text).
     const int j = vec - n_audio;
-    float bv = -INFINITY;
-    int bi = INT32_MAX;
-    for (int p = gt; p < sv.text_parts; p += TPV)
-      keep_better(bv, bi, sv.text_val[(size_t)j * sv.text_parts + p],
-                  sv.text_idx[(size_t)j * sv.text_parts + p]);
+    const int tparts = hv.T_text / kTextPartCols;   // T_text < V_text: a multiple of 32
+    const bool masked = hv.T_text < hv.V_text;
+    float bv = -INFINITY, av = -INFINITY;
+    int bi = INT32_MAX, ai = INT32_MAX;
+    for (int p = gt; p < sv.text_parts; p += TPV) {
+      const float v = sv.text_val[(size_t)j * sv.text_parts + p];
+      const int i = sv.text_idx[(size_t)j * sv.text_parts + p];
+      if (!masked || p < tparts) keep_better(bv, bi, v, i);
+      keep_better(av, ai, v, i);
+    }
     const int tok = grp_argmax_f32<TPV>(bv, bi, sm, slot);
+    int leave = 0;
+    if (masked) leave = grp_argmax_f32<TPV>(av, ai, sm, slot) >= hv.T_text;
     for (int kk = gt; kk < hv.K; kk += TPV)
       sv.tokens_out[(size_t)r * hv.K + kk] = (kk == 0) ? tok : hv.pad_id;
+    if (sv.modality_out && gt == 0) sv.modality_out[r] = (uint8_t)leave;
     return;
   }
   const int f = t - hv.delays.d[k];

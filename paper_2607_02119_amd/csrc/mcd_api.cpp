@@ -116,6 +116,7 @@ mcd_status make_step_view(const mcd_head *h, const mcd_step_args *a, bool need_h
   sv.seed = a->seed;
   sv.tokens_out = a->tokens_out;
   sv.frame_grid = a->frame_grid;
+  sv.modality_out = a->modality_out;
   sv.n_slots = a->n_slots;
   sv.F_max = a->F_max;
   sv.scores = a->scores;
@@ -193,6 +194,10 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
     vmax = vk > vmax ? vk : vmax;
   }
   if (vmax != d->V) return fail(MCD_E_INVALID, "V=%d is not the largest stream (%d)", d->V, vmax);
+  if (d->T_text < 0 || d->T_text > d->V_text ||
+      (d->T_text > 0 && d->T_text < d->V_text && d->T_text % mcd::kTextPartCols != 0))
+    return fail(MCD_E_UNSUPPORTED, "T_text=%d: 0, V_text or a multiple of %d below V_text",
+                d->T_text, mcd::kTextPartCols);
   mcd_head *h = new (std::nothrow) mcd_head;
   if (!h) return fail(MCD_E_INVALID, "out of host memory");
   h->hv.H = d->H;
@@ -207,6 +212,7 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
   h->hv.W_text = d->V_text > 0 ? d->W_text : nullptr;
   h->hv.delays = del;
   h->hv.voff = voff;
+  h->hv.T_text = (d->T_text > 0 && d->T_text < d->V_text) ? d->T_text : d->V_text;
   h->max_delay = max_d;
   *out = h;
   return MCD_OK;
@@ -354,6 +360,67 @@ mcd_status mcd_sample_step(const mcd_head *h, const mcd_step_args *a, hipStream_
   if (sv.R == 0) return MCD_OK;
   hipError_t e = mcd::launch_sample(h->hv, sv, true, stream);
   if (e != hipSuccess) return hip_fail(e, "sample launch");
+  return MCD_OK;
+}
+
+mcd_status mcd_phase_advance(const mcd_phase_desc *d, int32_t n, uint8_t *phase,
+                             int32_t *count, const int32_t *token0, const uint8_t *modality,
+                             int32_t *emit) {
+  if (!d || n < 0 || d->n_bridge < 0 || d->drain_steps < 0 || (d->n_bridge > 0 && !d->bridge))
+    return fail(MCD_E_INVALID, "bad phase description or n");
+  if (n == 0) return MCD_OK;
+  if (!phase || !count || !token0 || !modality || !emit) return fail(MCD_E_INVALID, "null array");
+  const int32_t nb = d->n_bridge;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t c = count[i];
+    int32_t ph = phase[i], nc = 0, out = -1;
+    switch (ph) {
+      case MCD_PHASE_TEXT:
+        if (c != 0) return fail(MCD_E_INVALID, "request %d: count %d in the text phase", i, c);
+        if (!modality[i]) {
+          out = token0[i];
+        } else if (nb == 0) {
+          out = token0[i];
+          ph = MCD_PHASE_AUDIO;
+        } else {
+          out = d->bridge[0];
+          ph = nb > 1 ? MCD_PHASE_BRIDGE : MCD_PHASE_AUDIO;
+          nc = nb > 1 ? 1 : 0;
+        }
+        break;
+      case MCD_PHASE_BRIDGE:
+        if (c < 1 || c >= nb) return fail(MCD_E_INVALID, "request %d: bridge count %d", i, c);
+        out = d->bridge[c];
+        if (c + 1 >= nb) {
+          ph = MCD_PHASE_AUDIO;
+        } else {
+          nc = c + 1;
+        }
+        break;
+      case MCD_PHASE_AUDIO:
+        if (c < 0) return fail(MCD_E_INVALID, "request %d: audio count %d", i, c);
+        if (token0[i] == d->audio_end) {
+          ph = d->drain_steps > 0 ? MCD_PHASE_DRAIN : MCD_PHASE_TEXT;
+        } else {
+          nc = c + 1;
+        }
+        break;
+      case MCD_PHASE_DRAIN:
+        if (c < 0 || c >= d->drain_steps)
+          return fail(MCD_E_INVALID, "request %d: drain count %d", i, c);
+        if (c + 1 >= d->drain_steps) {
+          ph = MCD_PHASE_TEXT;
+        } else {
+          nc = c + 1;
+        }
+        break;
+      default:
+        return fail(MCD_E_INVALID, "request %d: unknown phase %d", i, ph);
+    }
+    phase[i] = (uint8_t)ph;
+    count[i] = nc;
+    emit[i] = out;
+  }
   return MCD_OK;
 }
 

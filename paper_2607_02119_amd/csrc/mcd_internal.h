@@ -38,6 +38,7 @@ struct HeadView {
   const void *W_text;
   Delays delays;
   StreamOffsets voff;
+  int32_t T_text;       // text ids of the text head (the text phase's mask), V_text if none
 };
 
 // One step, by value in kernel arguments.
@@ -56,6 +57,7 @@ struct StepView {
   uint64_t seed;
   int32_t *tokens_out;
   int32_t *frame_grid;
+  uint8_t *modality_out;
   int32_t n_slots, F_max;
   float *scores;
   uint32_t *status;

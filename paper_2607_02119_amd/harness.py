@@ -38,11 +38,11 @@ class DeviceWorkload:
         W = to_device(hh["W"], device)
         Wt = None if hh["W_text"] is None else to_device(hh["W_text"], device)
         b = None if hh.get("bias") is None else to_device(hh["bias"], device)
-        vs = hh.get("V_stream")
-        self.heads = [mcd.Head(W, hh["delays"], hh["pad_id"], b, Wt, vs)]
+        vs, tt = hh.get("V_stream"), hh.get("T_text", 0)
+        self.heads = [mcd.Head(W, hh["delays"], hh["pad_id"], b, Wt, vs, tt)]
         for _ in range(1, weight_copies):
             self.heads.append(mcd.Head(W.clone(), hh["delays"], hh["pad_id"], b,
-                                       None if Wt is None else Wt.clone(), vs))
+                                       None if Wt is None else Wt.clone(), vs, tt))
         self.plan = self.heads[0].plan(self.layout["pair_map"], self.layout["row_kind"], device)
         R, K = wl.R, wl.K
         b0 = inputs.make_batch(wl, 0, self.layout)
@@ -54,6 +54,7 @@ class DeviceWorkload:
             .expand(self.steps, R).contiguous()
         self.hidden = None
         self.tokens = torch.full((R, K), -1, dtype=torch.int32, device=device)
+        self.modality = torch.full((R,), 255, dtype=torch.uint8, device=device)
         self.grid = torch.full((max(wl.n_slots, 1), K, max(wl.frames, 1)), -1, dtype=torch.int32,
                                device=device)
         self.scores = torch.zeros((max(wl.Rs, 1), wl.N), dtype=torch.float32, device=device)
@@ -79,7 +80,8 @@ class DeviceWorkload:
                     n_frames=p["n_frames"], grid_slot=p["grid_slot"], seed=self.seed,
                     tokens_out=self.tokens if tokens is None else tokens,
                     frame_grid=self.grid, n_slots=self.wl.n_slots, F_max=self.wl.frames,
-                    scores=self.scores if scores is None else scores, workspace=self.workspace)
+                    scores=self.scores if scores is None else scores, workspace=self.workspace,
+                    modality_out=self.modality)
 
     def run_step(self, t: int, hidden_index=None, copy=0, stream=None):
         """One decode step at step t with hidden state slot `hidden_index` (default t)."""

@@ -70,6 +70,7 @@ class Workload:
     pad_id: int | None = None    # default V
     bias: bool = False           # stream-embedding term b[k][v] (W_k e_k) of the heads
     V_stream: tuple | None = None  # ids per stream when they differ (V = the largest)
+    T_text: int = 0              # text ids of the text head (the text phase's mask), 0: all
 
     @property
     def R(self) -> int:
@@ -186,6 +187,8 @@ def make_weights(wl: Workload, seed_w: int = SEED_W) -> dict:
                 W=W, bias=bias, W_text=Wt)
     if wl.V_stream is not None:
         head["V_stream"] = np.array(sizes, np.int32)
+    if wl.T_text:
+        head["T_text"] = wl.T_text
     return head
 
 

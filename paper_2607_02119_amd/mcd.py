@@ -34,7 +34,7 @@ _i32 = ctypes.c_int32
 class mcd_head_desc(ctypes.Structure):
     _fields_ = [("H", _i32), ("K", _i32), ("V", _i32), ("pad_id", _i32),
                 ("delays", _vp), ("dtype", ctypes.c_int), ("W", _vp), ("bias", _vp),
-                ("V_text", _i32), ("W_text", _vp), ("V_stream", _vp)]
+                ("V_text", _i32), ("W_text", _vp), ("V_stream", _vp), ("T_text", _i32)]
 
 
 class mcd_batch_counts(ctypes.Structure):
@@ -46,7 +46,7 @@ class mcd_step_args(ctypes.Structure):
                 ("cfg_w", _vp), ("temperature", _vp), ("top_k", _vp), ("top_p", _vp),
                 ("rng_key", _vp), ("step", _vp), ("n_frames", _vp), ("grid_slot", _vp),
                 ("seed", ctypes.c_uint64), ("tokens_out", _vp), ("frame_grid", _vp),
-                ("n_slots", _i32), ("F_max", _i32), ("scores", _vp), ("workspace", _vp),
+                ("modality_out", _vp), ("n_slots", _i32), ("F_max", _i32), ("scores", _vp), ("workspace", _vp),
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
@@ -54,6 +54,10 @@ class mcd_next_input_args(ctypes.Structure):
     _fields_ = [("R", _i32), ("H", _i32), ("K", _i32), ("V", _i32), ("pad_id", _i32),
                 ("dtype", ctypes.c_int), ("E", _vp), ("V_text", _i32), ("E_text", _vp),
                 ("row_kind", _vp), ("tokens", _vp), ("out", _vp), ("workspace", _vp)]
+
+
+class mcd_phase_desc(ctypes.Structure):
+    _fields_ = [("n_bridge", _i32), ("bridge", _vp), ("audio_end", _i32), ("drain_steps", _i32)]
 
 
 def _sig(name, res, *args):
@@ -78,6 +82,8 @@ _mcd_head_logits = _sig("mcd_head_logits", ctypes.c_int, _vp, ctypes.POINTER(mcd
 _mcd_deinterleave = _sig("mcd_deinterleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _vp, _vp)
 _mcd_interleave = _sig("mcd_interleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _i32, _vp, _vp)
 _mcd_next_input = _sig("mcd_next_input", ctypes.c_int, ctypes.POINTER(mcd_next_input_args), _vp)
+_mcd_phase_advance = _sig("mcd_phase_advance", ctypes.c_int, ctypes.POINTER(mcd_phase_desc), _i32,
+                          _vp, _vp, _vp, _vp, _vp)
 _mcd_read_device_status = _sig("mcd_read_device_status", ctypes.c_int, _vp,
                                ctypes.POINTER(ctypes.c_uint32), _vp)
 _mcd_status_string = _sig("mcd_status_string", ctypes.c_char_p, ctypes.c_int)
@@ -86,7 +92,8 @@ _mcd_last_error = _sig("mcd_last_error", ctypes.c_char_p)
 EXPORTED = ["mcd_head_create", "mcd_head_destroy", "mcd_plan_words", "mcd_batch_plan",
             "mcd_plan_sampled_row", "mcd_workspace_bytes", "mcd_head_step", "mcd_head_logits",
             "mcd_sample_step",
-            "mcd_deinterleave", "mcd_interleave", "mcd_next_input", "mcd_read_device_status",
+            "mcd_deinterleave", "mcd_interleave", "mcd_phase_advance", "mcd_next_input",
+            "mcd_read_device_status",
             "mcd_status_string", "mcd_last_error"]
 
 
@@ -131,11 +138,11 @@ def mcd_last_error():
 
 
 def mcd_head_create(H, K, V, pad_id, delays, dtype, W, bias=None, V_text=0, W_text=None,
-                    V_stream=None):
+                    V_stream=None, T_text=0):
     d = np.ascontiguousarray(delays, dtype=np.int32)
     vs = None if V_stream is None else np.ascontiguousarray(V_stream, dtype=np.int32)
     desc = mcd_head_desc(H, K, V, pad_id, d.ctypes.data, dtype, _ptr(W), _ptr(bias), V_text,
-                         _ptr(W_text), _ptr(vs))
+                         _ptr(W_text), _ptr(vs), int(T_text))
     h = _vp()
     _check(_mcd_head_create(ctypes.byref(desc), ctypes.byref(h)), "mcd_head_create")
     return h
@@ -174,11 +181,11 @@ def mcd_workspace_bytes(h, R):
 
 def _step_args(R, counts, plan, hidden, cfg_w, temperature, top_k, top_p, rng_key, step,
                n_frames, grid_slot, seed, tokens_out, frame_grid, n_slots, F_max, scores,
-               workspace):
+               workspace, modality_out=None):
     return mcd_step_args(R, counts, _ptr(plan), _ptr(hidden), _ptr(cfg_w), _ptr(temperature),
                          _ptr(top_k), _ptr(top_p), _ptr(rng_key), _ptr(step), _ptr(n_frames),
-                         _ptr(grid_slot), seed, _ptr(tokens_out), _ptr(frame_grid), n_slots,
-                         F_max, _ptr(scores), _ptr(workspace),
+                         _ptr(grid_slot), seed, _ptr(tokens_out), _ptr(frame_grid),
+                         _ptr(modality_out), n_slots, F_max, _ptr(scores), _ptr(workspace),
                          0 if workspace is None else workspace.numel() * workspace.element_size())
 
 
@@ -225,6 +232,27 @@ def mcd_next_input(E, tokens, row_kind, pad_id, out, E_text=None, workspace=None
     _check(_mcd_next_input(ctypes.byref(a), _stream(stream)), "mcd_next_input")
 
 
+MCD_PHASE_TEXT, MCD_PHASE_BRIDGE, MCD_PHASE_AUDIO, MCD_PHASE_DRAIN = 0, 1, 2, 3
+
+
+def mcd_phase_advance(bridge, audio_end, drain_steps, phase, count, token0, modality):
+    """One step of the requests' phases (host arrays, updated in place):
+    phase uint8 [n], count int32 [n], token0 int32 [n], modality uint8 [n].
+    Returns emit int32 [n]."""
+    br = np.ascontiguousarray(bridge, dtype=np.int32)
+    d = mcd_phase_desc(br.shape[0], br.ctypes.data if br.shape[0] else None, int(audio_end),
+                       int(drain_steps))
+    for a, dt in ((phase, np.uint8), (count, np.int32)):
+        assert a.dtype == dt and a.flags.c_contiguous
+    token0 = np.ascontiguousarray(token0, dtype=np.int32)
+    modality = np.ascontiguousarray(modality, dtype=np.uint8)
+    emit = np.empty(phase.shape[0], dtype=np.int32)
+    _check(_mcd_phase_advance(ctypes.byref(d), phase.shape[0], phase.ctypes.data,
+                              count.ctypes.data, token0.ctypes.data, modality.ctypes.data,
+                              emit.ctypes.data), "mcd_phase_advance")
+    return emit
+
+
 def mcd_read_device_status(workspace, stream=None):
     code = ctypes.c_uint32()
     _check(_mcd_read_device_status(_ptr(workspace), ctypes.byref(code), _stream(stream)),
@@ -238,7 +266,7 @@ def mcd_read_device_status(workspace, stream=None):
 class Head:
     """Handle plus the device tensors it borrows."""
 
-    def __init__(self, W, delays, pad_id, bias=None, W_text=None, V_stream=None):
+    def __init__(self, W, delays, pad_id, bias=None, W_text=None, V_stream=None, T_text=0):
         """W: [K][V][H], or [N][H] with V_stream (the ids of each stream)."""
         assert W.is_cuda and W.is_contiguous()
         if V_stream is None:
@@ -254,7 +282,7 @@ class Head:
         self.delays = np.ascontiguousarray(delays, dtype=np.int32)
         self.V_text = 0 if W_text is None else W_text.shape[0]
         self.handle = mcd_head_create(H, K, V, self.pad_id, self.delays, dtype, W, bias,
-                                      self.V_text, W_text, V_stream)
+                                      self.V_text, W_text, V_stream, T_text)
 
     def __del__(self):
         h = getattr(self, "handle", None)

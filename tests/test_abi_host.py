@@ -145,3 +145,45 @@ def test_next_input_validation():
         a = _next_input_args(**ok_empty)
         assert mcd._mcd_next_input(ctypes.byref(a), None) == mcd.MCD_OK
     assert mcd._mcd_next_input(None, None) == mcd.MCD_E_INVALID
+
+
+def test_text_mask_validation():
+    h = _head(V_text=100, W_text=FAKE_W, T_text=64)
+    mcd.mcd_head_destroy(h)
+    for tt in (0, 100):
+        mcd.mcd_head_destroy(_head(V_text=100, W_text=FAKE_W, T_text=tt))
+    for tt in (-1, 50, 101, 96 + 32):
+        with pytest.raises(mcd.McdError):
+            _head(V_text=100, W_text=FAKE_W, T_text=tt)
+
+
+def test_phase_advance_matches_oracle():
+    """The library's host phase machine against the oracle's, over random
+    token and modality streams for many requests."""
+    import oracle
+    rng = np.random.default_rng(7)
+    for bridge, end, drain in (([900, 901, 902], 7, 3), ([], 5, 0), ([42], 3, 1)):
+        n = 64
+        phase = np.zeros(n, np.uint8)
+        count = np.zeros(n, np.int32)
+        ref = [(0, 0)] * n
+        seen = set()
+        for step in range(200):
+            tok = rng.integers(0, 10, size=n).astype(np.int32)
+            mod = (rng.random(n) < 0.1).astype(np.uint8)
+            emit = mcd.mcd_phase_advance(bridge, end, drain, phase, count, tok, mod)
+            for i in range(n):
+                ph, c, e = oracle.phase_advance(ref[i][0], ref[i][1], int(tok[i]), int(mod[i]),
+                                                bridge, end, drain)
+                ref[i] = (ph, c)
+                assert (phase[i], count[i], emit[i]) == (ph, c, e), (step, i)
+                seen.add(ph)
+        assert seen >= {oracle.PHASE_TEXT, oracle.PHASE_AUDIO}
+
+
+def test_phase_advance_rejects_bad_state():
+    for ph, c in ((9, 0), (0, 1), (1, 0), (1, 5), (3, 2), (2, -1)):
+        phase = np.array([ph], np.uint8)
+        count = np.array([c], np.int32)
+        with pytest.raises(mcd.McdError):
+            mcd.mcd_phase_advance([1, 2], 7, 2, phase, count, [0], [0])

@@ -60,6 +60,12 @@ def _check_step(dw, t, tc, rows=None, score_tol=None):
     b, o = _oracle_step(dw, t, rows)
     sel = np.arange(dw.wl.R) if rows is None else np.asarray(rows)
     tc.add(g_tok[sel], o["tokens"], o["flags"], where=f"t={t}")
+    # TEXT rows' modality flag (the unmasked argmax past the text ids), except
+    # where the two regions' maxima are within the score rounding
+    g_mod = _cpu(dw.modality)[sel]
+    for i, r in enumerate(sel):
+        if dw.layout["row_kind"][r] == inputs.ROW_TEXT and o["modality_gap"][i] >= GAP_TOL:
+            assert g_mod[i] == o["modality"][i], (t, int(r))
     if score_tol is not None and dw.wl.Rs:
         err = score_rel_err(g_sc, _plan_rows(dw, None if rows is None else list(sel)), o["scores"],
                             oracle.stream_sizes(dw.host_head))
@@ -136,6 +142,16 @@ RAGGED = [
                                   shuffle=True)),
     ("unequal_streams_f32", dict(H=40, K=3, V=37, V_stream=(37, 2, 20), n_pairs=3, n_solo=2,
                                  n_text=1, V_text=70, dtype="f32", top_p=0.8, steps=5)),
+    # the text phase's vocabulary mask (text ids [0, T_text)) and the modality
+    # inferred from the unmasked argmax, on the streaming, MFMA and fused paths
+    ("text_mask_stream", dict(H=256, K=3, V=37, n_pairs=10, n_solo=5, n_text=40, V_text=300,
+                              T_text=256, dtype="bf16", top_k=7, steps=5, shuffle=True)),
+    ("text_mask_mfma", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=3000,
+                            T_text=2048, dtype="bf16", top_k=5, steps=3, shuffle=True)),
+    ("text_mask_fused", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, n_text=70, V_text=900,
+                             T_text=64, dtype="bf16", top_k=15, steps=9, shuffle=True)),
+    ("text_mask_f32", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=4, V_text=70,
+                           T_text=32, dtype="f32", top_k=5, steps=4, shuffle=True)),
     # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
     ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
                                 temperature=0.9, steps=4, shuffle=True)),
