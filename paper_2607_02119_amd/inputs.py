@@ -131,6 +131,17 @@ WORKLOADS = {
                        temperature=0.8, top_k=20, steps=256),
     "cfg_off": Workload("cfg_off", H=4096, K=16, V=1024, n_pairs=0, n_solo=512, cfg_w=3.0,
                         temperature=0.8, top_k=20, steps=256),
+    # Two shapes of the next rows, beside the benchmark table: nine streams of
+    # unequal size as in OpusLM's 1 SSL + 8 codec streams (Sec. 3.1; the sizes
+    # are assumed: 4096 ids for the first stream, 1024 for the others), and
+    # the mixed batch with the text phase's vocabulary mask (the last 4096
+    # text-head ids stand for the other modality's markers; Sec. 2.2).
+    "opuslm_9_streams": Workload("opuslm_9_streams", H=4096, K=9, V=4096,
+                                 V_stream=(4096,) + (1024,) * 8, n_pairs=64, cfg_w=2.0,
+                                 temperature=1.0, top_p=0.95, steps=512),
+    "mixed_text_mask": Workload("mixed_text_mask", H=4096, K=8, V=4096, n_pairs=256, n_solo=256,
+                                n_text=128, V_text=151936, T_text=151936 - 4096, cfg_w=3.0,
+                                temperature=1.0, top_k=50, steps=128, shuffle=True),
 }
 # index order of the benchmark's configuration list
 CONFIG_INDEX = ["tiny_ref", "memory_bound_decode", "weight_streaming", "mfma_mixed", "cfg_on"]

@@ -450,7 +450,8 @@ def test_device_status_bad_parameter_pads_and_flags():
 # Benchmark-sized workloads: GPU on the whole batch, the oracle on sampled rows.
 
 FULL = [("memory_bound_decode", [7, 130, 253]), ("weight_streaming", [7, 300, 511]),
-        ("mfma_mixed", [7, 125]), ("cfg_on", [15, 250]), ("cfg_off", [15])]
+        ("mfma_mixed", [7, 125]), ("cfg_on", [15, 250]), ("cfg_off", [15]),
+        ("opuslm_9_streams", [9, 300]), ("mixed_text_mask", [9])]
 
 
 @pytest.mark.parametrize("name,steps", FULL, ids=[f[0] for f in FULL])
