@@ -177,7 +177,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the head stage is single-GPU in this build)", file=sys.stderr)
+              "(the head stage is measured on one GPU)", file=sys.stderr)
         sys.exit(2)
 
     import torch
