@@ -204,9 +204,9 @@ struct Smem {
   } u;
   // elements of the cut bin (at most TPV)
   Entry le[TPV];
+  uint32_t nkw[5];                       // the vector's noise key, from its first wave
   uint32_t keepbits[TPV];                // kept cut-bin elements, one bit per slot of a thread
   uint32_t lcount;
-  uint32_t nkw[5];                       // the vector's noise key, from its first wave
   // reductions across the waves of a group (two slots, alternating, one barrier each)
   uint32_t ru[2][Grp<TPV>::kGW];
   unsigned long long r64[2][Grp<TPV>::kGW];
@@ -499,6 +499,30 @@ __device__ __forceinline__ NoiseKey noise_key(uint64_t seed, uint64_t rng_key, i
   const U64x4 d = philox4x64(0, (uint64_t)k, (uint64_t)t, rng_key, seed);
   return NoiseKey{(uint32_t)d.w[0], (uint32_t)(d.w[0] >> 32), (uint32_t)d.w[1],
                   (uint32_t)(d.w[1] >> 32), (uint32_t)d.w[2]};
+}
+
+// A uniform 32-bit value copied to a vector register, so that what is
+// computed from it runs on the vector unit.
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t x) {
+  uint32_t y;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "s"(x));
+  return y;
+}
+
+// The same key computed by every wave on the vector unit, whose 32 x 32 -> 64
+// multiply-adds shorten the chain of 64-bit products that the scalar unit
+// would run one 32-bit half at a time; the result is uniform again.
+__device__ __forceinline__ NoiseKey noise_key_vector_unit(uint64_t seed, uint64_t rng_key, int t,
+                                                          int k) {
+  auto v64 = [](uint64_t x) __attribute__((always_inline)) {
+    return ((uint64_t)in_vgpr((uint32_t)(x >> 32)) << 32) | in_vgpr((uint32_t)x);
+  };
+  const U64x4 d = philox4x64(0, (uint64_t)in_vgpr((uint32_t)k), (uint64_t)in_vgpr((uint32_t)t),
+                             v64(rng_key), v64(seed));
+  auto s32 = [](uint64_t x) __attribute__((always_inline)) {
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  };
+  return NoiseKey{s32(d.w[0]), s32(d.w[0] >> 32), s32(d.w[1]), s32(d.w[1] >> 32), s32(d.w[2])};
 }
 
 struct U32x4 {
@@ -1056,7 +1080,8 @@ __device__ __forceinline__ int draw_nucleus(const float (&x)[4 * GPT], uint32_t 
 template <int GPT, int TPV>
 __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (&x)[4 * GPT],
                                                uint32_t active, int V, bool greedy, int top_k,
-                                               float top_p, Smem<TPV> &sm, int &slot) {
+                                               float top_p, const NoiseKey &nk_in,
+                                               Smem<TPV> &sm, int &slot) {
   constexpr int EPL = 4 * GPT;
   const int gt = Grp<TPV>::tid();
   uint32_t mk = 0;
@@ -1080,8 +1105,10 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     return (int)grp_min_u32<TPV>(id, sm, slot);
   }
   const float mx = key_to_float(mk);
-  // the noise key, published by the barrier of the maximum
-  const NoiseKey nk{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
+  // a workgroup group's key, published by its first wave before the barrier
+  // of the maximum
+  NoiseKey nk = nk_in;
+  if constexpr (TPV != kWave) nk = NoiseKey{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
   int pass = 0;
   bool u_dirty = false;
   uint32_t kept = active;
@@ -1242,26 +1269,34 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
     if (bad) {
       if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PARAM);
     } else {
-      // The vector's noise key: 64-bit multiplies on uniform values (scalar
-      // unit); one wave derives it for the group and publishes it in LDS.
-      if (T != 0.0f && Grp<TPV>::wave() == 0) {
-        const NoiseKey nk = noise_key(sv.seed, rkey, t, k);
+      // The vector's noise key (64-bit multiplies on uniform values).  A
+      // one-wave group derives it on the vector unit (a shorter chain than the
+      // scalar unit's 32-bit halves).  In a workgroup group the first wave
+      // derives it on the scalar unit, beside the other waves' vector work,
+      // and publishes it in LDS; the first group barrier makes it visible
+      // (the maximum's in the top-k path, the one below otherwise).
+      NoiseKey nk{0, 0, 0, 0, 0};
+      if constexpr (TPV == kWave) {
+        if (T != 0.0f) nk = noise_key_vector_unit(sv.seed, rkey, t, k);
+      } else if (T != 0.0f && Grp<TPV>::wave() == 0) {
+        const NoiseKey w0 = noise_key(sv.seed, rkey, t, k);
         if (lane_id() == 0) {
-          sm.nkw[0] = nk.k0;
-          sm.nkw[1] = nk.k1;
-          sm.nkw[2] = nk.c1;
-          sm.nkw[3] = nk.c2;
-          sm.nkw[4] = nk.c3;
+          sm.nkw[0] = w0.k0;
+          sm.nkw[1] = w0.k1;
+          sm.nkw[2] = w0.c1;
+          sm.nkw[3] = w0.c2;
+          sm.nkw[4] = w0.c3;
         }
       }
       if (T != 0.0f && !(top_k > 0 && top_k < V)) {
         // no top-k cut: candidates in perturbed-score order tested against the
-        // nucleus (the noise of every id, drawn once the key is published)
+        // nucleus (the noise of every id)
         Grp<TPV>::sync();
-        const NoiseKey nk{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
+        if constexpr (TPV != kWave)
+          nk = NoiseKey{sm.nkw[0], sm.nkw[1], sm.nkw[2], sm.nkw[3], sm.nkw[4]};
         token = draw_nucleus<GPT, TPV>(x, active, nk, P, sm, slot);
       } else {
-        token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, sm, slot);
+        token = select_and_draw<GPT, TPV>(sv, x, active, V, T == 0.0f, top_k, P, nk, sm, slot);
       }
       sampled = true;
     }
