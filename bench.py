@@ -8,7 +8,10 @@ draw, pads, companion copy, frame-grid scatter) over one batch of the workload.
 Inputs are resident in HBM before timing; the timed loop walks the workload's
 decode steps (each with its own hidden states and step index) and rotates
 through several copies of the weights so that they stream from HBM rather than
-from the 256 MB Infinity Cache.
+from the 256 MB Infinity Cache.  The timed launches are issued one by one
+(--graphs captures them in HIP graphs beforehand and replays those instead;
+the step time came out the same and the weight-streaming projection read a
+few microseconds slower per launch, so replay is not the default).
 
 Prints one JSON line: value = client-visible codebook tokens per second
 (sampled rows x codebooks per step / step time), the roofline of the head
@@ -166,6 +169,8 @@ def main():
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="weight_streaming")
+    ap.add_argument("--graphs", action="store_true",
+                    help="replay the timed launches from HIP graphs captured beforehand")
     ap.add_argument("--no-next-input", action="store_true",
                     help="skip the timing of the next-step input kernel")
     ap.add_argument("--weight-copies", type=int, default=0,
@@ -203,36 +208,52 @@ def main():
         step(i)
     torch.cuda.synchronize()
     status = dw.status()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    ms_step = ev0.elapsed_time(ev1) / args.steps
-    status |= dw.status()
 
-    # mean launch duration of each of the two kernels: the same steps launched
-    # back to back on the launch stream, HIP events at both ends
-    def per_launch(fn):
+    def timed(fn):
+        """Mean ms per call of fn(i), i = warmup .. warmup + steps - 1, back to
+        back on the launch stream between HIP events: issued one by one, or,
+        with --graphs, captured beforehand in HIP graphs of up to 50 calls each
+        and replayed once each (the same launches, without the host's
+        per-call cost)."""
+        calls = [args.warmup + i for i in range(args.steps)]
+        graphs = []
+        if args.graphs:
+            for c0 in range(0, len(calls), 50):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    for i in calls[c0:c0 + 50]:
+                        fn(i, None)
+                graphs.append(g)
+            torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
         a.record(stream)
-        for i in range(args.steps):
-            fn(args.warmup + i)
+        if not args.graphs:
+            for i in calls:
+                fn(i, stream)
+        else:
+            for g in graphs:
+                g.replay()
         b.record(stream)
         torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps
+        return a.elapsed_time(b) / len(calls)
 
-    def logits(i):
+    def step_fn(i, st):
         t = i % n_hidden
-        dw.run_logits(t, hidden_index=t, copy=i % copies, stream=stream)
+        dw.run_step(t, hidden_index=t, copy=i % copies, stream=st)
 
-    def sample(i):
-        dw.run_sample(i % n_hidden, copy=i % copies, stream=stream)
+    # the whole step, then each of the two kernels alone over the same steps
+    def logits(i, st):
+        t = i % n_hidden
+        dw.run_logits(t, hidden_index=t, copy=i % copies, stream=st)
 
-    ms_k1 = per_launch(logits)
-    ms_k2 = per_launch(sample)
+    def sample(i, st):
+        dw.run_sample(i % n_hidden, copy=i % copies, stream=st)
+
+    ms_step = timed(step_fn)
+    status |= dw.status()
+    ms_k1 = timed(logits)
+    ms_k2 = timed(sample)
     status |= dw.status()
 
     # the next row of the path: the next-step input built from the last
