@@ -17,9 +17,9 @@
 //   * the token goes to the Main row, to its Companion (Sec. 2.4) and to the
 //     request's frame grid cell [k][f].
 //
-// Layout: thread tid owns groups g = q * 256 + tid of four consecutive ids
-// 4g .. 4g + 3 (one 16-byte load each), so that one Philox4x32 block serves a
-// whole group from registers.
+// Layout: thread tid of a vector's TPV threads owns groups g = q * TPV + tid of
+// four consecutive ids 4g .. 4g + 3 (one 16-byte load each), so that one
+// Philox4x32 block serves a whole group from registers.
 //
 // Selection.  Every score s falls in a bin b = floor(16 (max - s)) (bins of
 // width 1/16 below the maximum, the last one open-ended); the bin index is

@@ -236,6 +236,10 @@ SAMPLER = [
     (4096, 4, 8, 1.0, 0.25, 1.0, 0, 0.3),        # small p, heavy ties: several candidates
     (1000, 2, 3, 0.0, 0.0, 1.0, 0, 0.5),         # all scores equal: the nucleus is by id
     (37, 3, 5, 1.0, 0.5, 1.0, 37, 0.7),          # top-k = V is no cut
+    # workgroup per vector with two and four groups of ids per thread, over
+    # more vectors than compute units
+    (2048, 8, 72, 3.6, 0.0, 0.9, 50, 1.0),
+    (4096, 8, 72, 2.24, 0.0, 1.0, 0, 0.95),
     # at least 1024 vectors of at most 1024 ids: one wave per vector
     (1024, 16, 64, 3.6, 0.0, 0.8, 20, 1.0),
     (512, 8, 128, 2.24, 0.0, 1.0, 0, 0.95),
@@ -290,6 +294,7 @@ EXACT_BOUNDARY = [
     (64, 4, 64, 0.5),             # workgroup per vector, one group of ids per thread
     (64, 4, 256, 0.5),            # one wave per vector
     (4096, 4, 8, 8 / 4096),       # workgroup per vector, four groups per thread
+    (4096, 8, 72, 8 / 4096),      # the same over more vectors than compute units
     (1024, 4, 256, 16 / 1024),    # one wave per vector, four groups per thread
 ]
 
