@@ -283,11 +283,15 @@ class Head:
         self.V_text = 0 if W_text is None else W_text.shape[0]
         self.handle = mcd_head_create(H, K, V, self.pad_id, self.delays, dtype, W, bias,
                                       self.V_text, W_text, V_stream, T_text)
+        # the library's own entry, held here: at interpreter exit the module's
+        # globals may already be gone when this object is collected
+        self._destroy = _mcd_head_destroy
 
     def __del__(self):
         h = getattr(self, "handle", None)
-        if h is not None:
-            mcd_head_destroy(h)
+        destroy = getattr(self, "_destroy", None)
+        if h is not None and destroy is not None:
+            destroy(h)
             self.handle = None
 
     def plan(self, pair_map, row_kind, device="cuda"):
