@@ -267,6 +267,79 @@ typedef struct {
 mcd_status mcd_next_input(const mcd_next_input_args *args, hipStream_t stream);
 
 /* Synchronises `stream`, returns the status word in *code and clears it. */
+/* ---- paired co-scheduling (Sec. 2.4 input allocation and co-scheduling) ---
+ * [host] A continuous-batching scheduler for CFG requests; no HIP calls.
+ *   - Auto-allocation: a request with cfg_w > 1 becomes a unit of two rows, its
+ *     Main row and a Companion row with a null prompt; other requests are
+ *     one-row units.
+ *   - Atomic unit: a unit is admitted with all its rows or not at all, holds
+ *     them until it finishes, and its rows finish together.
+ *   - Equal budget: in a step, each member of a pair is granted the same
+ *     number of prompt tokens, c = min(floor(left / 2), the larger remaining
+ *     prompt), and the pair is charged 2c whether or not the shorter prompt
+ *     uses its share.
+ *   - CFG only in the audio phase (Sec. 3.4): a decoding request first emits text_len
+ *     text tokens (its Main row is a TEXT row of the head; the Companion is
+ *     not run), then n_frames + drain_steps audio steps (Main COND and
+ *     Companion UNCOND rows, or one SOLO row).  The Companion joins the audio
+ *     phase with a copy of the Main sequence (a prefix-cache hit: no prompt
+ *     tokens).
+ * One step: mcd_sched_plan builds the batch (decode rows of running units
+ * first, one token each; then prompt chunks of prefilling units in admission
+ * order; then strict first-come admission while rows and budget remain), and
+ * mcd_sched_commit applies it.  A unit whose prompts complete in a step
+ * decodes from the next step on. */
+typedef struct mcd_sched mcd_sched;
+
+typedef struct {
+  int32_t max_rows;          /* rows of the batch (Main and Companion rows), >= 1 */
+  int32_t token_budget;      /* backbone tokens per step, >= max_rows */
+  int32_t null_prompt_len;   /* prompt tokens of a Companion, >= 1 */
+  int32_t drain_steps;       /* audio steps after the last frame (largest delay), >= 0 */
+  int32_t max_requests;      /* requests held at once (waiting and running), >= 1 */
+} mcd_sched_desc;
+
+typedef struct {
+  float cfg_w;               /* > 1: a pair with a Companion */
+  int32_t prompt_len;        /* >= 1 */
+  int32_t text_len;          /* text tokens before the audio, >= 0 */
+  int32_t n_frames;          /* audio frames, >= 1 */
+} mcd_sched_request;
+
+/* The planned step; the arrays belong to the scheduler and stay valid until
+ * the next mcd_sched_plan or mcd_sched_destroy. */
+typedef struct {
+  int32_t n_rows;            /* backbone rows of the step (rows with tokens) */
+  const int32_t *row_req;    /* [n_rows] request id */
+  const uint8_t *row_member; /* [n_rows] 0 Main, 1 Companion */
+  const int32_t *row_slot;   /* [n_rows] the row's slot in [0, max_rows) */
+  const int32_t *row_tokens; /* [n_rows] tokens this step (prompt chunk, or 1) */
+  const int32_t *row_context;/* [n_rows] tokens already in the row's context */
+  int32_t R;                 /* head rows: the decoding rows, in backbone order */
+  const int32_t *head_row;   /* [R] backbone row of each head row */
+  const int32_t *pair_map;   /* [R] head index of the partner, -1 */
+  const uint8_t *row_kind;   /* [R] MCD_ROW_* */
+  const float *cfg_w;        /* [R] */
+  const int32_t *step;       /* [R] audio step (text rows: text step) */
+  const int32_t *n_frames;   /* [R] */
+  const int32_t *grid_slot;  /* [R] Main's slot for audio Main/SOLO rows, else -1 */
+} mcd_sched_batch;
+
+mcd_status mcd_sched_create(const mcd_sched_desc *desc, mcd_sched **out);
+void mcd_sched_destroy(mcd_sched *s);
+/* Queue a request; *id receives its id (0, 1, ... in submission order).
+ * MCD_E_INVALID for bad fields, a pair on a one-row batch, or a full table. */
+mcd_status mcd_sched_submit(mcd_sched *s, const mcd_sched_request *req, int32_t *id);
+/* Plan the next step.  MCD_E_INVALID if the last planned step is not yet
+ * committed. */
+mcd_status mcd_sched_plan(mcd_sched *s, mcd_sched_batch *out);
+/* Apply the planned step.  The ids of the requests that finished with it go
+ * to finished[0 .. *n_finished) (at most cap; MCD_E_INVALID and nothing
+ * applied if more would finish). */
+mcd_status mcd_sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_t *n_finished);
+/* Requests waiting and running. */
+mcd_status mcd_sched_counts(const mcd_sched *s, int32_t *waiting, int32_t *running);
+
 mcd_status mcd_read_device_status(void *workspace, uint32_t *code, hipStream_t stream);
 
 const char *mcd_status_string(mcd_status s);

@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libmcd.so")
 ARCH = "gfx950"
 
 SOURCES = ["mcd_api.cpp", "k_head_gemm.hip", "k_stream.hip", "k_mfma.hip", "k_fused.hip", "k_sample.hip",
-           "k_grid.hip", "k_embed.hip"]
+           "k_grid.hip", "k_embed.hip", "mcd_sched.cpp"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra",

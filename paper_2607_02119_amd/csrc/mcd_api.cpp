@@ -504,3 +504,5 @@ mcd_status mcd_read_device_status(void *workspace, uint32_t *code, hipStream_t s
 }
 
 }  // extern "C"
+
+mcd_status mcd::record_error(mcd_status s, const char *msg) { return fail(s, "%s", msg); }

@@ -95,6 +95,8 @@ struct EmbedView {
   uint32_t *status;          // or null
 };
 hipError_t launch_next_input(const EmbedView &ev, bool bf16, hipStream_t stream);
+// Records a host-side error for mcd_last_error and returns s (mcd_api.cpp).
+mcd_status record_error(mcd_status s, const char *msg);
 hipError_t launch_sample(const HeadView &hv, const StepView &sv, bool with_text,
                          hipStream_t stream);
 hipError_t launch_deinterleave(const int32_t *streams, int32_t n_req, int32_t T, int32_t K,

@@ -60,6 +60,23 @@ class mcd_phase_desc(ctypes.Structure):
     _fields_ = [("n_bridge", _i32), ("bridge", _vp), ("audio_end", _i32), ("drain_steps", _i32)]
 
 
+class mcd_sched_desc(ctypes.Structure):
+    _fields_ = [("max_rows", _i32), ("token_budget", _i32), ("null_prompt_len", _i32),
+                ("drain_steps", _i32), ("max_requests", _i32)]
+
+
+class mcd_sched_request(ctypes.Structure):
+    _fields_ = [("cfg_w", ctypes.c_float), ("prompt_len", _i32), ("text_len", _i32),
+                ("n_frames", _i32)]
+
+
+class mcd_sched_batch(ctypes.Structure):
+    _fields_ = [("n_rows", _i32), ("row_req", _vp), ("row_member", _vp), ("row_slot", _vp),
+                ("row_tokens", _vp), ("row_context", _vp), ("R", _i32), ("head_row", _vp),
+                ("pair_map", _vp), ("row_kind", _vp), ("cfg_w", _vp), ("step", _vp),
+                ("n_frames", _vp), ("grid_slot", _vp)]
+
+
 def _sig(name, res, *args):
     f = getattr(_lib, name)
     f.restype = res
@@ -70,6 +87,15 @@ def _sig(name, res, *args):
 _mcd_head_create = _sig("mcd_head_create", ctypes.c_int, ctypes.POINTER(mcd_head_desc),
                         ctypes.POINTER(_vp))
 _mcd_head_destroy = _sig("mcd_head_destroy", None, _vp)
+_mcd_sched_create = _sig("mcd_sched_create", ctypes.c_int, ctypes.POINTER(mcd_sched_desc),
+                         ctypes.POINTER(_vp))
+_mcd_sched_destroy = _sig("mcd_sched_destroy", None, _vp)
+_mcd_sched_submit = _sig("mcd_sched_submit", ctypes.c_int, _vp,
+                         ctypes.POINTER(mcd_sched_request), ctypes.POINTER(_i32))
+_mcd_sched_plan = _sig("mcd_sched_plan", ctypes.c_int, _vp, ctypes.POINTER(mcd_sched_batch))
+_mcd_sched_commit = _sig("mcd_sched_commit", ctypes.c_int, _vp, _vp, _i32, ctypes.POINTER(_i32))
+_mcd_sched_counts = _sig("mcd_sched_counts", ctypes.c_int, _vp, ctypes.POINTER(_i32),
+                         ctypes.POINTER(_i32))
 _mcd_plan_words = _sig("mcd_plan_words", ctypes.c_size_t, _i32)
 _mcd_batch_plan = _sig("mcd_batch_plan", ctypes.c_int, _vp, _i32, _vp, _vp, _vp, ctypes.c_size_t,
                        ctypes.POINTER(mcd_batch_counts))
@@ -94,6 +120,8 @@ EXPORTED = ["mcd_head_create", "mcd_head_destroy", "mcd_plan_words", "mcd_batch_
             "mcd_sample_step",
             "mcd_deinterleave", "mcd_interleave", "mcd_phase_advance", "mcd_next_input",
             "mcd_read_device_status",
+            "mcd_sched_create", "mcd_sched_destroy", "mcd_sched_submit", "mcd_sched_plan",
+            "mcd_sched_commit", "mcd_sched_counts",
             "mcd_status_string", "mcd_last_error"]
 
 
@@ -251,6 +279,71 @@ def mcd_phase_advance(bridge, audio_end, drain_steps, phase, count, token0, moda
                               count.ctypes.data, token0.ctypes.data, modality.ctypes.data,
                               emit.ctypes.data), "mcd_phase_advance")
     return emit
+
+
+class Scheduler:
+    """Paired co-scheduling of CFG requests (host only): the C scheduler of
+    libmcd behind plan() / commit()."""
+
+    _I32 = ("row_req", "row_slot", "row_tokens", "row_context", "head_row", "pair_map", "step",
+            "n_frames", "grid_slot")
+
+    def __init__(self, max_rows, token_budget, null_prompt_len, drain_steps, max_requests=4096):
+        d = mcd_sched_desc(int(max_rows), int(token_budget), int(null_prompt_len),
+                           int(drain_steps), int(max_requests))
+        h = _vp()
+        _check(_mcd_sched_create(ctypes.byref(d), ctypes.byref(h)), "mcd_sched_create")
+        self.handle = h.value
+        self.max_requests = int(max_requests)
+        self._destroy = _mcd_sched_destroy
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        destroy = getattr(self, "_destroy", None)
+        if h is not None and destroy is not None:
+            destroy(h)
+            self.handle = None
+
+    def submit(self, cfg_w, prompt_len, text_len, n_frames):
+        q = mcd_sched_request(float(cfg_w), int(prompt_len), int(text_len), int(n_frames))
+        rid = _i32()
+        _check(_mcd_sched_submit(self.handle, ctypes.byref(q), ctypes.byref(rid)),
+               "mcd_sched_submit")
+        return rid.value
+
+    def plan(self):
+        """The next step as a dict of numpy copies (backbone rows and head rows)."""
+        b = mcd_sched_batch()
+        _check(_mcd_sched_plan(self.handle, ctypes.byref(b)), "mcd_sched_plan")
+
+        def arr(name, n, ct, dt):
+            p = getattr(b, name)
+            if n == 0 or not p:
+                return np.zeros(0, dtype=dt)
+            return np.ctypeslib.as_array(ctypes.cast(p, ctypes.POINTER(ct)), (n,)).astype(dt)
+
+        out = {"n_rows": b.n_rows, "R": b.R}
+        for name in self._I32:
+            n = b.R if name in ("head_row", "pair_map", "step", "n_frames", "grid_slot") else b.n_rows
+            out[name] = arr(name, n, ctypes.c_int32, np.int32)
+        out["row_member"] = arr("row_member", b.n_rows, ctypes.c_uint8, np.uint8)
+        out["row_kind"] = arr("row_kind", b.R, ctypes.c_uint8, np.uint8)
+        out["cfg_w"] = arr("cfg_w", b.R, ctypes.c_float, np.float32)
+        return out
+
+    def commit(self):
+        """Apply the planned step; returns the ids of the requests it finished."""
+        fin = np.empty(self.max_requests, dtype=np.int32)
+        n = _i32()
+        _check(_mcd_sched_commit(self.handle, fin.ctypes.data, fin.shape[0], ctypes.byref(n)),
+               "mcd_sched_commit")
+        return fin[:n.value].copy()
+
+    def counts(self):
+        w, r = _i32(), _i32()
+        _check(_mcd_sched_counts(self.handle, ctypes.byref(w), ctypes.byref(r)),
+               "mcd_sched_counts")
+        return w.value, r.value
 
 
 def mcd_read_device_status(workspace, stream=None):
