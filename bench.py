@@ -163,6 +163,130 @@ def cpu_baseline(wl, budget_s=15.0):
                        f"({tokens} codebook tokens), {elapsed:.1f} s single-threaded fp64")
 
 
+# Stand-in backbone of the co-scheduling simulation: a memory-bound decoder
+# step of an 8B-parameter model with grouped KV heads (36 layers, 8 KV heads
+# of 128 dimensions): its bf16 weights once per step, and the bf16 K and V of
+# every context token of every row.
+STANDIN_WEIGHT_BYTES = 16.4e9
+STANDIN_KV_BYTES_PER_TOKEN = 36 * 8 * 128 * 2 * 2
+
+
+def cosched(args, torch):
+    """Paired co-scheduling over a stand-in backbone (closed loop, one GPU).
+
+    The library's host scheduler plans every step; a stand-in backbone step
+    reads the bytes such a step reads (weights, and the K/V of every context
+    token); the head step (K1 + K2 on this library's kernels) runs on the
+    step's decoding rows, with hidden states from a fixed random pool.  CFG on:
+    `--cosched-requests` / 2 requests with w = 3 (Main + Companion); CFG off:
+    as many solo requests as rows.  Each side keeps its requests in flight
+    (a finished request is replaced at once), runs `--warmup` steps, then times
+    `--cosched-steps` steps after `--cosched-warmup`.  Prints one JSON line with
+    both sides and their ratio."""
+    import numpy as np
+    from paper_2607_02119_amd import mcd
+
+    H, K, V, V_text, D = 4096, 8, 4096, 151936, 7
+    rows = args.cosched_requests
+    dev = "cuda"
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(17)
+    W = (torch.randn((K, V, H), generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+    W_text = (torch.randn((V_text, H), generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+    head = mcd.Head(W, delays=np.arange(K, dtype=np.int32), pad_id=V, W_text=W_text)
+    pool = (torch.randn((rows, H), generator=gen, device=dev)).to(torch.bfloat16)
+    F_max = 320
+    scores = torch.empty((rows, K * V), dtype=torch.float32, device=dev)
+    tokens = torch.empty((rows, K), dtype=torch.int32, device=dev)
+    grid = torch.full((rows, K, F_max), -1, dtype=torch.int32, device=dev)
+    modality = torch.empty(rows, dtype=torch.uint8, device=dev)
+    workspace = head.workspace(rows, dev)
+    buf = torch.zeros(4 << 30, dtype=torch.bfloat16, device=dev)    # 8 GiB read by the stand-in
+
+    def backbone(nbytes):
+        n = int(nbytes) // 2
+        while n > 0:
+            k = min(n, buf.numel())
+            buf[:k].amax()
+            n -= k
+
+    rng = np.random.default_rng(5)
+
+    def new_request(s, cfg_w):
+        # TTS-like requests: a prompt, a text preamble, then 2-6 s of audio at 50 frames/s
+        return s.submit(cfg_w, int(rng.integers(100, 401)), int(rng.integers(100, 401)),
+                        int(rng.integers(100, 301)))
+
+    def run(cfg_on):
+        n_req = rows // 2 if cfg_on else rows
+        s = mcd.Scheduler(rows, 8192, 16, D, max_requests=2 * n_req)
+        info = {}
+        for _ in range(n_req):
+            new_request(s, 3.0 if cfg_on else 1.0)
+        client, frames, host_s = 0, 0, 0.0
+        stream = torch.cuda.current_stream()
+        t0 = None
+        warm, steps = args.cosched_warmup, args.cosched_steps
+        for it in range(warm + steps):
+            if it == warm:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                client, frames, host_s = 0, 0, 0.0
+            h0 = time.perf_counter()
+            b = s.plan()
+            host_s += time.perf_counter() - h0
+            backbone(STANDIN_WEIGHT_BYTES + STANDIN_KV_BYTES_PER_TOKEN *
+                     float(np.sum(b["row_context"]) + np.sum(b["row_tokens"])))
+            R = b["R"]
+            if R:
+                kinds = b["row_kind"]
+                plan = head.plan(b["pair_map"], kinds, dev)
+                up = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+                rk = b["row_req"][b["head_row"]].astype(np.uint64)
+                mcd.mcd_head_step(
+                    head.handle, stream=stream, R=R, counts=plan.counts, plan=plan.dev,
+                    hidden=pool[:R], cfg_w=up(b["cfg_w"]),
+                    temperature=up(np.ones(R, np.float32)),
+                    top_k=up(np.full(R, 50, np.int32)), top_p=up(np.ones(R, np.float32)),
+                    rng_key=up(rk), step=up(b["step"]), n_frames=up(b["n_frames"]),
+                    grid_slot=up(b["grid_slot"]), seed=1234, tokens_out=tokens,
+                    frame_grid=grid, n_slots=rows, F_max=F_max, scores=scores,
+                    workspace=workspace, modality_out=modality)
+                main = kinds != mcd.MCD_ROW_UNCOND
+                client += int(np.sum(main))
+                frames += int(np.sum(main & (kinds != mcd.MCD_ROW_TEXT)))
+            h0 = time.perf_counter()
+            fin = s.commit()
+            host_s += time.perf_counter() - h0
+            for _ in fin:
+                new_request(s, 3.0 if cfg_on else 1.0)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        st = mcd.mcd_read_device_status(workspace)
+        info.update(requests_in_flight=n_req, ms_per_step=round(el / steps * 1e3, 3),
+                    client_tokens_per_s=round(client / el, 1),
+                    audio_steps_per_s=round(frames / el, 1),
+                    host_scheduler_us_per_step=round(host_s / steps * 1e6, 2),
+                    device_status=st)
+        return info
+
+    on = run(True)
+    print(f"cosched: CFG on done, {on['ms_per_step']} ms per step", file=sys.stderr, flush=True)
+    off = run(False)
+    print(f"cosched: CFG off done, {off['ms_per_step']} ms per step", file=sys.stderr, flush=True)
+    print(json.dumps({
+        "metric": "co-scheduled client decode tokens/s, CFG on / off",
+        "value": round(on["client_tokens_per_s"] / off["client_tokens_per_s"], 4),
+        "unit": "ratio", "higher_is_better": True, "n_gpus": 1, "steps": args.cosched_steps,
+        "warmup": args.cosched_warmup, "data": "synthetic",
+        "config": {"workload": f"cosched: {rows} rows, budget 8192, prompt 100-400, text "
+                               "100-400, frames 100-300, K 8 x V 4096, text head 151936, "
+                               "H 4096, bf16",
+                   "stand_in": {"weight_bytes": STANDIN_WEIGHT_BYTES,
+                                "kv_bytes_per_token": STANDIN_KV_BYTES_PER_TOKEN}},
+        "cfg_on": on, "cfg_off": off}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -179,6 +303,13 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device copy first (counter calibration)")
+    ap.add_argument("--cosched", action="store_true",
+                    help="run the paired co-scheduling simulation instead of the head step")
+    ap.add_argument("--cosched-requests", type=int, default=512,
+                    help="rows of the co-scheduled batch")
+    ap.add_argument("--cosched-steps", type=int, default=1500)
+    ap.add_argument("--cosched-warmup", type=int, default=600,
+                    help="untimed steps first, so that the requests in flight are at all stages")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -186,6 +317,11 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.cosched:
+        torch.cuda.set_device(0)
+        cosched(args, torch)
+        return
 
     from paper_2607_02119_amd import harness, inputs
 
