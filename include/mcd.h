@@ -288,7 +288,8 @@ mcd_status mcd_next_input(const mcd_next_input_args *args, hipStream_t stream);
  * first, one token each; then prompt chunks of prefilling units in admission
  * order; then strict first-come admission while rows and budget remain), and
  * mcd_sched_commit applies it.  A unit whose prompts complete in a step
- * decodes from the next step on. */
+ * decodes from the next step on.  A scheduler is not thread-safe: one caller
+ * at a time. */
 typedef struct mcd_sched mcd_sched;
 
 typedef struct {
