@@ -187,3 +187,17 @@ def test_phase_advance_rejects_bad_state():
         count = np.array([c], np.int32)
         with pytest.raises(mcd.McdError):
             mcd.mcd_phase_advance([1, 2], 7, 2, phase, count, [0], [0])
+
+
+def test_empty_batch_is_a_no_op():
+    """A step over no rows returns OK before any launch (no pointer is read)."""
+    h = _head()
+    c = mcd.mcd_batch_counts(0, 0, 0)
+    a = mcd.mcd_step_args(0, c, None, None, None, None, None, None, None, None, None, None, 0,
+                          None, None, None, 0, 0, None, FAKE_W, 256)
+    for name, f in [("mcd_head_step", mcd._mcd_head_step),
+                    ("mcd_head_logits", mcd._mcd_head_logits),
+                    ("mcd_sample_step", mcd._mcd_sample_step)]:
+        rc = f(h, ctypes.byref(a), None)
+        assert rc == mcd.MCD_OK, (name, mcd.mcd_last_error())
+    mcd.mcd_head_destroy(h)

@@ -98,6 +98,9 @@ def test_tiny_ref_full_run_tokens_scores_grid():
 
 RAGGED = [
     # name, workload kwargs
+    # the largest head the library takes: 32 codebooks of 4096 ids (delays 0..31)
+    ("max_k_max_v", dict(H=64, K=32, V=4096, n_pairs=3, n_solo=2, dtype="bf16", top_k=50,
+                         cfg_w=2.0, steps=35)),
     ("bf16_ragged_mixed", dict(H=128, K=3, V=37, n_pairs=70, n_solo=5, n_text=3, V_text=300,
                                dtype="bf16", top_k=7, temperature=0.7, steps=6, shuffle=True)),
     ("bf16_topp_two_tiles", dict(H=192, K=2, V=333, n_pairs=20, n_solo=3, dtype="bf16",
