@@ -122,7 +122,11 @@ mcd_status mcd_sched_create(const mcd_sched_desc *desc, mcd_sched **out) {
 
 void mcd_sched_destroy(mcd_sched *s) { delete s; }
 
-mcd_status mcd_sched_submit(mcd_sched *s, const mcd_sched_request *q, int32_t *id) {
+}  // extern "C"
+
+namespace {
+
+mcd_status sched_submit(mcd_sched *s, const mcd_sched_request *q, int32_t *id) {
   if (!s || !q || !id) return bad("null scheduler, request or id");
   if (!std::isfinite(q->cfg_w) || q->prompt_len < 1 || q->text_len < 0 || q->n_frames < 1)
     return bad("bad request (finite cfg_w, prompt >= 1, text >= 0, frames >= 1)");
@@ -145,7 +149,7 @@ mcd_status mcd_sched_submit(mcd_sched *s, const mcd_sched_request *q, int32_t *i
   return MCD_OK;
 }
 
-mcd_status mcd_sched_plan(mcd_sched *s, mcd_sched_batch *out) {
+mcd_status sched_plan(mcd_sched *s, mcd_sched_batch *out) {
   if (!s || !out) return bad("null scheduler or output");
   if (s->planned) return bad("the planned step is not committed yet");
   const size_t n = s->reqs.size();
@@ -223,7 +227,7 @@ mcd_status mcd_sched_plan(mcd_sched *s, mcd_sched_batch *out) {
   return MCD_OK;
 }
 
-mcd_status mcd_sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_t *n_finished) {
+mcd_status sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_t *n_finished) {
   if (!s || !n_finished || cap < 0 || (cap > 0 && !finished))
     return bad("null scheduler, output or bad capacity");
   if (!s->planned) return bad("no planned step to commit");
@@ -258,6 +262,36 @@ mcd_status mcd_sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_
   s->planned = false;
   *n_finished = nf;
   return MCD_OK;
+}
+
+}  // namespace
+
+// No exception crosses the C ABI: a failed host allocation becomes an error
+// code, after which the scheduler's state is unspecified (destroy it).
+extern "C" {
+
+mcd_status mcd_sched_submit(mcd_sched *s, const mcd_sched_request *q, int32_t *id) {
+  try {
+    return sched_submit(s, q, id);
+  } catch (...) {
+    return mcd::record_error(MCD_E_INVALID, "out of host memory");
+  }
+}
+
+mcd_status mcd_sched_plan(mcd_sched *s, mcd_sched_batch *out) {
+  try {
+    return sched_plan(s, out);
+  } catch (...) {
+    return mcd::record_error(MCD_E_INVALID, "out of host memory");
+  }
+}
+
+mcd_status mcd_sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_t *n_finished) {
+  try {
+    return sched_commit(s, finished, cap, n_finished);
+  } catch (...) {
+    return mcd::record_error(MCD_E_INVALID, "out of host memory");
+  }
 }
 
 mcd_status mcd_sched_counts(const mcd_sched *s, int32_t *waiting, int32_t *running) {
