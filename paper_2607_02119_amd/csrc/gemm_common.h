@@ -136,7 +136,7 @@ __device__ inline float4 pair_params(const StepView &sv, const int32_t *rows, in
 // bias, applies the CFG merge (Eq. 1) and 1/T, and stores 16 bytes per output
 // row.  Text: each thread scans whole 32-column parts of rows and writes the
 // (max, lowest argmax) partials.  Starts with a workgroup barrier.
-template <int BM, int BN, int CP, bool TEXT, int NH>
+template <int BM, int BN, int CP, bool TEXT, int NH, int NT = 256>
 __device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const StepView &sv,
                                                   const float *C, const float4 *rowp, int m0,
                                                   int n0, int M, int N) {
@@ -148,8 +148,8 @@ __device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const Step
   };
   if constexpr (!TEXT) {
     constexpr int CH = BN / 4;
-    constexpr int ITEMS = (BM / 2) * CH / 256;
-    static_assert(ITEMS >= 1 && (BM / 2) * CH % 256 == 0, "whole items per thread");
+    constexpr int ITEMS = (BM / 2) * CH / NT;
+    static_assert(ITEMS >= 1 && (BM / 2) * CH % NT == 0, "whole items per thread");
     const int c = tid % CH;
     const int nc = n0 + 4 * c;
     floatx4 bias = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -174,7 +174,7 @@ __device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const Step
     };
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const int q = (it * 256 + tid) / CH;
+      const int q = (it * NT + tid) / CH;
       if (m0 + 2 * q >= M || nc >= N) continue;
       const float *c0 = C + (2 * q) * CP + 4 * c;
       const floatx4 v0 = sum4(c0) + bias;
@@ -195,7 +195,7 @@ __device__ __forceinline__ void epilogue_from_lds(const HeadView &hv, const Step
     static_assert(kTextPartCols == 32 && BN % 32 == 0, "text parts are 32 columns");
     constexpr int PPR = BN / 32;
     __syncthreads();
-    for (int item = tid; item < BM * PPR; item += 256) {
+    for (int item = tid; item < BM * PPR; item += NT) {
       const int row = item / PPR, p = item % PPR;
       const int g = m0 + row;
       const int part = (n0 + 32 * p) / kTextPartCols;

@@ -7,16 +7,18 @@ namespace mcd {
 namespace {
 
 // MFMA-regime path for more than 128 GEMM rows (bf16, H a multiple of 32).
-// A workgroup owns a 256 x 128 output tile.  The waves split it by row half
-// (wm = wave & 1) and k half (kh = wave >> 1): each wave accumulates a
-// 128 x 128 block (4 x 4 blocks of v_mfma_f32_32x32x16_bf16, 256 accumulator
-// registers) over its 16 k of every 32-k slice, so each MFMA costs half a
-// fragment of LDS reads.  Slices are copied global->LDS like the streaming
-// path: waves 0-1 copy weight slices into a deep ring (the weights come from
-// HBM, once per XCD), waves 2-3 copy hidden-state slices into a shorter one
+// A workgroup owns a 256 x 128 output tile with eight waves, two per SIMD, so
+// that one wave's MFMAs cover the other's LDS reads and copies.  The waves
+// split it by row half (wm = wave & 1), column half (wn = (wave >> 1) & 1) and
+// k half (kh = wave >> 2): each wave accumulates a 128 x 64 block (4 x 2
+// blocks of v_mfma_f32_32x32x16_bf16, 128 accumulator registers) over its
+// 16 k of every 32-k slice.  Slices are copied global->LDS like the streaming
+// path: waves 0-3 copy weight slices into a deep ring (the weights come from
+// HBM, once per XCD), waves 4-7 copy hidden-state slices into a shorter one
 // (they are re-read from L2).  A slice row is 64 bytes, 4 chunks of 16 B;
 // chunk c of row r is stored at position c ^ ((r >> 2) & 3), so the 16 rows
-// of a 16-lane fragment read group hit all 64 banks once.
+// of a 16-lane fragment read group hit all 64 banks once.  (WAVES = 4 is the
+// one-wave-per-SIMD form: 128 x 128 blocks per wave.)
 //
 // Tile order is XCD-aware: workgroups are dealt to the 8 XCDs in turn, so the
 // grid index is remapped to give each XCD a contiguous run of tiles, in which
@@ -24,23 +26,30 @@ namespace {
 // they share that column's weights through the XCD's L2.
 constexpr int kMfmaBM = 256, kMfmaBN = 128, kMfmaSK = 32;
 constexpr int kMfmaSA = 5, kMfmaSB = 8;
+constexpr int kMfmaWaves = 8;
 
-template <bool TEXT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void head_gemm_mfma(
-    HeadView hv, StepView sv) {
+template <bool TEXT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WAVES / 4, WAVES / 4)))
+void head_gemm_mfma(HeadView hv, StepView sv) {
   constexpr int BM = kMfmaBM, BN = kMfmaBN, SK = kMfmaSK;
   constexpr int SA = kMfmaSA, SB = kMfmaSB;
+  constexpr int NTH = 64 * WAVES;                    // threads
+  constexpr int CW = WAVES / 4;                      // column groups of waves (1 or 2)
+  constexpr int HW = WAVES / 2;                      // waves per copy role
   constexpr int ROWB = SK * 2;                       // 64 bytes per row and slice
   constexpr int AST = BM * ROWB, BST = BN * ROWB;    // 16 KiB, 8 KiB per stage
-  constexpr int AIA = AST / 1024 / 2, BIB = BST / 1024 / 2;  // copies per wave per slice
-  constexpr int MB = 4, NB = 4;                      // 32x32 blocks per wave
+  constexpr int AIA = AST / 1024 / HW, BIB = BST / 1024 / HW;  // copies per wave per slice
+  constexpr int MB = 4, NB = 4 / CW;                 // 32x32 blocks per wave
+  constexpr int WNC = BN / CW;                       // columns per wave
+  static_assert(WAVES == 4 || WAVES == 8, "one or two waves per SIMD");
   static_assert((SA - 1) * AIA < 64 && (SB - 1) * BIB < 64, "vmcnt range");
   // both copy roles keep the same number of copies in flight in the loop, so
   // that its one wait needs no branch (a branch makes the compiler's own
   // LDS-read waits conservative)
   constexpr int kLoopVm = (SA - 2) * AIA;
   static_assert((SB - 2) * BIB == kLoopVm, "equal in-flight copy counts");
-  static_assert(MB * NB == 16 && AIA == 8 && BIB == 4, "copy slots of the slice schedule");
+  static_assert(AIA * 2 == MB * NB && BIB * 4 == MB * NB && MB + NB <= MB * NB,
+                "copy and fragment slots of the slice schedule");
   constexpr int CP = BN + 4;                         // epilogue row pitch (floats)
   static_assert(BM * CP * 4 <= SA * AST + SB * BST, "epilogue tile fits the rings");
 
@@ -63,9 +72,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int tile_m = bx % tiles_m, tile_n = bx / tiles_m;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, kh = wave >> 1;
+  const int wm = wave & 1, wn = (wave >> 1) & (CW - 1), kh = wave / (2 * CW);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const bool b_copier = wave_s < 2;
+  const bool b_copier = wave_s < HW;
 
   // the row tiles of one column tile walk k in the same order (they share the
   // weights in L2); different column tiles start at different k
@@ -91,7 +100,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const uint32_t sb = abase + (uint32_t)((st % SA) * AST);
     static_for<0, AIA>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
-      lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+      lds_copy16(src[q] + ks * SK, sb + (uint32_t)(((wave_s - HW) * AIA + q) * 1024));
     });
   };
 
@@ -121,7 +130,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       constexpr int q = decltype(qc)::value;
       src[q] = nullptr;
       if (q < AIA) {
-        const int r = ((wave_s - 2) * AIA + q) * 16 + seg_r;
+        const int r = ((wave_s - HW) * AIA + q) * 16 + seg_r;
         int pr = rows[min(m0 + r, M - 1)];
         if (pr < 0 || pr >= sv.R) {
           atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
@@ -130,8 +139,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         src[q] = X + (size_t)pr * H + ((seg_p ^ ((r >> 2) & 3)) * 8);
       }
     });
-    const int q2 = tid - 128;
-    if (!TEXT) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
+    const int q2 = tid - NTH / 2;
+    if (!TEXT && q2 < BM / 2) rowp[q2] = pair_params(sv, rows, m0 + 2 * q2);
     wait_vmem_and_lds<0>();
 #pragma unroll
     for (int st = 0; st < SA; ++st) issue_a(st);
@@ -156,7 +165,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const int r = j * 32 + frow;
+    const int r = wn * WNC + j * 32 + frow;
     boff[j] = r * ROWB + ((fch ^ ((r >> 2) & 3)) * 16);
   }
 
@@ -200,11 +209,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       if constexpr (m < MB) na[m] = *reinterpret_cast<const bf16x8 *>(asb + aoff[m]);
       else if constexpr (m < MB + NB) nb[m - MB] = *reinterpret_cast<const bf16x8 *>(bsb + boff[m - MB]);
       if constexpr (m % 2 == 1) {
-        constexpr int q = m / 2;           // A copies 0..7 after the odd MFMAs
-        if (!b_copier) lds_copy16(src[q] + ks * SK, csb + (uint32_t)(((wave_s - 2) * AIA + q) * 1024));
+        constexpr int q = m / 2;           // A copies after the odd MFMAs
+        if (!b_copier) lds_copy16(src[q] + ks * SK, csb + (uint32_t)(((wave_s - HW) * AIA + q) * 1024));
       }
       if constexpr (m % 4 == 3) {
-        constexpr int q = m / 4;           // B copies 0..3 after every fourth
+        constexpr int q = m / 4;           // B copies after every fourth
         if (b_copier) lds_copy16(src[q] + ks * SK, csb + (uint32_t)((wave_s * BIB + q) * 1024));
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -227,7 +236,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // every thread applies the fused epilogue to 16-byte column chunks.
   float *C = reinterpret_cast<float *>(lds);
   // element (i, j, r) of this lane sits at Cl + a compile-time offset
-  float *Cl = C + (wm * 128 + (lane >> 5) * 4) * CP + frow;
+  float *Cl = C + (wm * 128 + (lane >> 5) * 4) * CP + wn * WNC + frow;
   if (kh == 1) {
     static_for<0, MB * NB * 16>([&](auto fc) __attribute__((always_inline)) {
       constexpr int f = decltype(fc)::value;
@@ -245,7 +254,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       Cl[off] = acc[i][j][r] + Cl[off];
     });
   }
-  epilogue_from_lds<BM, BN, CP, TEXT, 1>(hv, sv, C, rowp, m0, n0, M, N);
+  epilogue_from_lds<BM, BN, CP, TEXT, 1, NTH>(hv, sv, C, rowp, m0, n0, M, N);
 }
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void head_gemm_mfma2(
@@ -262,8 +271,10 @@ hipError_t launch_mfma2(const HeadView &hv, const StepView &sv, hipStream_t st) 
 
 template <bool TEXT>
 hipError_t launch_mfma(const HeadView &hv, const StepView &sv, int M, int N, hipStream_t st) {
+  constexpr int WAVES = kMfmaWaves;
   const int tm = (M + kMfmaBM - 1) / kMfmaBM, tn = (N + kMfmaBN - 1) / kMfmaBN;
-  hipLaunchKernelGGL((head_gemm_mfma<TEXT>), dim3(tm * tn), dim3(256), 0, st, hv, sv);
+  hipLaunchKernelGGL((head_gemm_mfma<TEXT, WAVES>), dim3(tm * tn), dim3(64 * WAVES), 0, st, hv,
+                     sv);
   return hipGetLastError();
 }
 
