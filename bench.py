@@ -50,8 +50,8 @@ MEASURED_TRAFFIC = {
     # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
     "weight_streaming": dict(
         sources=["k_stream.hip", "stream_tile.h", "gemm_common.h"],
-        sha256="87dab1027e57cc3ff7ac62d89794f12552fb83db4fd0f0a0ace85aa525ce70e3",
-        fetch_bytes=277193933, write_bytes=8388608,
+        sha256="f026eec05ce4811440c25fa305ca150d277aa4042f56379e7b223732309f1849",
+        fetch_bytes=277193114, write_bytes=8388608,
         profile="profiles/head_step_weight_streaming.md"),
 }
 
