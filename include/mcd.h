@@ -9,8 +9,12 @@
  *   - the in-batch CFG merge of each conditional (Main) row with its
  *     unconditional (Companion) partner, w * l_cond + (1 - w) * l_uncond, per
  *     codebook (Eq. 1), only for audio rows (Sec. 2.4);
- *   - temperature, top-k and top-p selection and a Gumbel-max draw keyed by a
- *     counter-based Philox4x64-10 generator, for all K streams of a row in the
+ *   - temperature, top-k and top-p selection and a Gumbel-max draw from a
+ *     counter-based generator in two levels (Philox, Salmon et al., SC'11):
+ *     once per (row, codebook, step) vector, Philox4x64-10 with key (seed, 0)
+ *     and counter (0, k, t, rng_key) gives the key material D; id v then takes
+ *     word v mod 4 of Philox4x32-10 with key (lo D0, hi D0) and counter
+ *     (v / 4, lo D1, hi D1, lo D2).  All K streams of a row are drawn in the
  *     same step (synchronous multi-stream sampling, Sec. 2.3);
  *   - the delay pattern: codebook k at step t carries frame t - d_k (Sec. 2.1);
  *     positions with no frame (before the stream starts, or in the drain that
@@ -31,7 +35,8 @@
  *     non-OK return.  No call aborts or throws.  Conditions only the device can
  *     see (a parameter value out of range, a grid cell outside the grid, a
  *     corrupt plan) set bits of a sticky status word in the workspace and make
- *     the affected outputs the pad id; read it with mcd_read_device_status.
+ *     the affected tokens the pad id (the grid cell is then not written); read
+ *     it with mcd_read_device_status.
  *   - Calls that share a workspace must not overlap in time.
  */
 #ifndef MCD_H
@@ -95,11 +100,14 @@ typedef struct {
   const void *W_text;        /* [V_text][H] or NULL */
   const int32_t *V_stream;   /* [host][K] ids of each stream (1..MCD_MAX_V), or NULL;
                                 copied at creation */
-  int32_t T_text;            /* text-phase vocabulary mask (Sec. 2.2): ids [0, T_text) of the
+  int32_t T_text;            /* text-phase vocabulary mask (Sec. 2.3): ids [0, T_text) of the
                                 text head are text tokens, the rest mark other modalities.
                                 0 or V_text: no mask; else a multiple of 32 below V_text */
 } mcd_head_desc;
 
+/* Creates the handle.  A bf16 head with a text head also creates, on the
+ * current device, the second stream and the two events its mixed batches use
+ * (MCD_E_HIP if that fails); nothing is created later, in a step. */
 mcd_status mcd_head_create(const mcd_head_desc *desc, mcd_head **out);
 void mcd_head_destroy(mcd_head *head);
 
@@ -138,7 +146,10 @@ typedef struct {
   mcd_batch_counts counts;   /* as returned by mcd_batch_plan */
   const int32_t *plan;       /* device copy of the plan words */
   const void *hidden;        /* [R][H] of the head's dtype, 16-byte aligned */
-  const float *cfg_w;        /* [R] CFG scale, read on COND rows (any finite w) */
+  /* Per-row arrays, [R] each: every one is required when R > 0 (MCD_E_INVALID
+     otherwise), whatever the row kinds, since the kernels read them at every
+     row; only rng_key may be NULL. */
+  const float *cfg_w;        /* [R] CFG scale, used on COND rows (any finite w) */
   const float *temperature;  /* [R] >= 0; 0 selects greedy decoding */
   const int32_t *top_k;      /* [R] <= 0 or >= V: no top-k */
   const float *top_p;        /* [R] in (0, 1); >= 1: no top-p */
@@ -196,7 +207,7 @@ mcd_status mcd_interleave(const int32_t *grid, int32_t n_req, int32_t F, int32_t
                           const int32_t *delays /*[host][K]*/, int32_t pad_id,
                           int32_t *streams, hipStream_t stream);
 
-/* ---- mixed-modality phases (Sec. 2.2) -------------------------------------
+/* ---- mixed-modality phases (Sec. 2.3) -------------------------------------
  * Each request moves through a text phase (TEXT rows: greedy over the text
  * ids, the mask of mcd_head_desc.T_text), a transition that injects
  * deterministic bridging tokens, an audio phase (audio rows: all K streams),
@@ -266,7 +277,6 @@ typedef struct {
  * MCD_DEV_BAD_TOKEN in the workspace status word (when a workspace is given). */
 mcd_status mcd_next_input(const mcd_next_input_args *args, hipStream_t stream);
 
-/* Synchronises `stream`, returns the status word in *code and clears it. */
 /* ---- paired co-scheduling (Sec. 2.4 input allocation and co-scheduling) ---
  * [host] A continuous-batching scheduler for CFG requests; no HIP calls.
  *   - Auto-allocation: a request with cfg_w > 1 becomes a unit of two rows, its
@@ -341,6 +351,9 @@ mcd_status mcd_sched_commit(mcd_sched *s, int32_t *finished, int32_t cap, int32_
 /* Requests waiting and running. */
 mcd_status mcd_sched_counts(const mcd_sched *s, int32_t *waiting, int32_t *running);
 
+/* ---- device status ----------------------------------------------------------
+ * Synchronises `stream`, returns the status word of the workspace in *code
+ * (MCD_DEV_* bits) and clears it. */
 mcd_status mcd_read_device_status(void *workspace, uint32_t *code, hipStream_t stream);
 
 const char *mcd_status_string(mcd_status s);

@@ -343,7 +343,7 @@ def next_input(E, tokens, row_kind, pad_id, E_text=None):
 
 
 # --------------------------------------------------------------------------
-# Mixed-modality phase of a request (Sec. 2.2)
+# Mixed-modality phase of a request (Sec. 2.3)
 
 PHASE_TEXT, PHASE_BRIDGE, PHASE_AUDIO, PHASE_DRAIN = 0, 1, 2, 3
 

@@ -53,7 +53,7 @@ typedef struct {
    * sum_{j<k} V_stream[j], and N = sum_k V_stream[k].  NULL: V for every
    * stream, N = K * V. */
   const int32_t *V_stream;    /* [K] or NULL */
-  /* Text-phase vocabulary mask (Sec. 2.2): ids [0, T_text) of the text head
+  /* Text-phase vocabulary mask (Sec. 2.3): ids [0, T_text) of the text head
    * are text tokens, the rest belong to other modalities.  A TEXT row emits
    * the greedy token over the text ids only; its modality is read from the
    * unmasked distribution: 1 when the argmax over all V_text ids (lowest id

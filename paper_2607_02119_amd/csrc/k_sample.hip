@@ -1228,17 +1228,23 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(HeadView hv, StepView 
   const uint64_t rkey = sv.rng_key ? ld_const(sv.rng_key, rc) : (uint64_t)rc;
   const int gslot = ld_const(sv.grid_slot, rc);
 
-  if (!plan_good) {
-    if (vec == 0 && gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
-    return;
-  }
-  if (!row_ok) {
+  if (!plan_good || !row_ok) {
+    // A plan that does not match the step: flag it and make this vector's
+    // outputs the pad id wherever its rows are inside the batch, so stale
+    // tokens of an earlier step are never left in place.
     if (gt == 0) atomicOr(sv.status, (uint32_t)MCD_DEV_BAD_PLAN);
+    const bool r_in = r >= 0 && r < sv.R, u_in = u >= 0 && u < sv.R;
+    if (audio) {
+      if (gt == 0 && r_in) sv.tokens_out[(size_t)r * hv.K + k] = hv.pad_id;
+      if (gt == 0 && u_in) sv.tokens_out[(size_t)u * hv.K + k] = hv.pad_id;
+    } else if (r_in) {
+      for (int kk = gt; kk < hv.K; kk += TPV) sv.tokens_out[(size_t)r * hv.K + kk] = hv.pad_id;
+    }
     return;
   }
   if (!audio) {
     // text row: reduce the (max, lowest argmax) partials of the text GEMM.
-    // The text phase's mask (Sec. 2.2): the token is the best over the text
+    // The text phase's mask (Sec. 2.3): the token is the best over the text
     // ids [0, T_text), whole 32-column parts; the modality is where the best
     // over all ids lies (text ids are the lower ones, so ties stay text).
     const int j = vec - n_audio;

@@ -1,7 +1,7 @@
 // Host side of libmcd: argument validation, the batch plan and kernel launches.
 // Nothing here allocates device memory or synchronises, except
-// mcd_read_device_status.  A head creates one extra stream and two events the
-// first time it runs a batch with both audio and text rows.
+// mcd_read_device_status.  A head with a bf16 text head creates one extra
+// stream and two events at creation (mcd_head_create), never in a step.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -20,10 +20,12 @@ struct mcd_head {
   int32_t max_delay;
   // Batches with both audio and text rows run the two projections
   // concurrently: the text part on a second stream of the head, forked from
-  // and joined back to the caller's stream with events (created on first use).
+  // and joined back to the caller's stream with events.  Created with the
+  // head (bf16 heads with a text head), so a step creates nothing; the mutex
+  // orders the event records of concurrent steps on one head.
   mutable std::mutex side_mu;
-  mutable hipStream_t side = nullptr;
-  mutable hipEvent_t fork = nullptr, join = nullptr;
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 
 namespace {
@@ -51,11 +53,14 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-size_t text_bytes(const mcd_head *h, int32_t rows) {
-  if (h->hv.V_text <= 0) return 0;
+
+// Bytes of the text partials of n text rows: the values, then the ids, each
+// rounded up to 256 bytes.
+size_t partials_bytes(const mcd_head *h, int64_t n) {
+  if (h->hv.V_text <= 0 || n <= 0) return 0;
   const size_t parts = (size_t)mcd::text_parts_for(h->hv.V_text);
-  return round_up((size_t)rows * parts * sizeof(float), 256) +
-         round_up((size_t)rows * parts * sizeof(int32_t), 256);
+  return round_up((size_t)n * parts * sizeof(float), 256) +
+         round_up((size_t)n * parts * sizeof(int32_t), 256);
 }
 
 // Shared validation of mcd_head_step / mcd_sample_step; fills the step view.
@@ -80,12 +85,12 @@ mcd_status make_step_view(const mcd_head *h, const mcd_step_args *a, bool need_h
     if (hv.dtype == MCD_F32 && !aligned(a->hidden, 4))
       return fail(MCD_E_INVALID, "hidden must be 4-byte aligned");
   }
-  if (Rs > 0) {
-    if (!a->temperature || !a->top_k || !a->top_p || !a->step || !a->n_frames || !a->grid_slot)
-      return fail(MCD_E_INVALID, "a per-row parameter array is null");
-    if (c.n_pairs > 0 && !a->cfg_w) return fail(MCD_E_INVALID, "cfg_w is null");
-    if (!a->scores) return fail(MCD_E_INVALID, "scores is null");
-  }
+  // The kernels read every per-row array at every row (text rows included), so
+  // a non-empty batch needs all of them; rng_key alone may be null.
+  if (a->R > 0 && (!a->cfg_w || !a->temperature || !a->top_k || !a->top_p || !a->step ||
+                   !a->n_frames || !a->grid_slot))
+    return fail(MCD_E_INVALID, "a per-row parameter array is null");
+  if (Rs > 0 && !a->scores) return fail(MCD_E_INVALID, "scores is null");
   if (a->R > 0 && !a->tokens_out) return fail(MCD_E_INVALID, "tokens_out is null");
   if (a->n_slots < 0 || a->F_max < 0) return fail(MCD_E_INVALID, "negative grid size");
   if (a->frame_grid && (int64_t)a->n_slots * hv.K * a->F_max > ((int64_t)1 << 40))
@@ -214,6 +219,15 @@ mcd_status mcd_head_create(const mcd_head_desc *d, mcd_head **out) {
   h->hv.voff = voff;
   h->hv.T_text = (d->T_text > 0 && d->T_text < d->V_text) ? d->T_text : d->V_text;
   h->max_delay = max_d;
+  if (d->dtype == MCD_BF16 && d->V_text > 0) {
+    hipError_t e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      mcd_head_destroy(h);
+      return hip_fail(e, "side stream of the text projection");
+    }
+  }
   *out = h;
   return MCD_OK;
 }
@@ -300,7 +314,7 @@ mcd_status mcd_plan_sampled_row(const int32_t *plan, int32_t s, int32_t *row, in
 
 size_t mcd_workspace_bytes(const mcd_head *h, int32_t R) {
   if (!h) return 0;
-  return (size_t)mcd::kStatusBytes + text_bytes(h, R > 0 ? R : 0);
+  return (size_t)mcd::kStatusBytes + partials_bytes(h, R);
 }
 
 namespace {
@@ -315,13 +329,8 @@ hipError_t run_head_gemm(const mcd_head *h, const mcd::StepView &sv, hipStream_t
   bool fused = false;
   hipError_t e = mcd::launch_mixed_gemm(h->hv, sv, stream, &fused);
   if (fused || e != hipSuccess) return e;
+  if (!h->side) return hipErrorInvalidHandle;   // created with every bf16 text head
   std::lock_guard<std::mutex> lock(h->side_mu);
-  if (!h->side) {
-    e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
-    if (e != hipSuccess) return e;
-  }
   if ((e = hipEventRecord(h->fork, stream)) != hipSuccess) return e;
   if ((e = hipStreamWaitEvent(h->side, h->fork, 0)) != hipSuccess) return e;
   if ((e = mcd::launch_head_gemm_part(h->hv, sv, false, stream)) != hipSuccess) return e;

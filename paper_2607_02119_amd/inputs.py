@@ -135,7 +135,7 @@ WORKLOADS = {
     # unequal size as in OpusLM's 1 SSL + 8 codec streams (Sec. 3.1; the sizes
     # are assumed: 4096 ids for the first stream, 1024 for the others), and
     # the mixed batch with the text phase's vocabulary mask (the last 4096
-    # text-head ids stand for the other modality's markers; Sec. 2.2).
+    # text-head ids stand for the other modality's markers; Sec. 2.3).
     "opuslm_9_streams": Workload("opuslm_9_streams", H=4096, K=9, V=4096,
                                  V_stream=(4096,) + (1024,) * 8, n_pairs=64, cfg_w=2.0,
                                  temperature=1.0, top_p=0.95, steps=512),

@@ -57,8 +57,14 @@ def test_head_create_validation():
             _head(V_stream=vs, V=50)
 
 
+# A bf16 head with a text head creates its side stream (a HIP call) at
+# creation; the host-only tests take fp32 heads where a text head is needed.
+def _text_head(**kw):
+    return _head(dtype=mcd.MCD_F32, H=40, V_text=100, W_text=FAKE_W, **kw)
+
+
 def test_batch_plan_layout_and_errors():
-    h = _head(V_text=100, W_text=FAKE_W)
+    h = _text_head()
     # rows: 0 solo, 1 uncond(->3), 2 text, 3 cond(->1), 4 cond(->5), 5 uncond(->4)
     pm = [-1, 3, -1, 1, 5, 4]
     rk = [2, 1, 3, 0, 0, 1]
@@ -110,6 +116,29 @@ def test_step_argument_errors_before_launch():
     assert rc == mcd.MCD_E_INVALID and "aligned" in mcd.mcd_last_error()
 
 
+def test_every_per_row_array_is_required():
+    """The kernels read every per-row parameter array at every row, text rows
+    included: a non-empty batch without one of them is rejected on the host,
+    whatever its row kinds (solo-only without cfg_w, text-only batches)."""
+    per_row = ("cfg_w", "temperature", "top_k", "top_p", "step", "n_frames", "grid_slot")
+    h = _text_head()
+    for pm, rk in (([-1, -1], [2, 2]),          # solo rows only
+                   ([-1, -1], [3, 3]),          # text rows only
+                   ([1, 0, -1], [0, 1, 3])):    # a pair and a text row
+        plan, c = mcd.mcd_batch_plan(h, pm, rk)
+        base = dict(R=len(pm), counts=c, plan=FAKE_W, hidden=FAKE_W, cfg_w=FAKE_W,
+                    temperature=FAKE_W, top_k=FAKE_W, top_p=FAKE_W, rng_key=None, step=FAKE_W,
+                    n_frames=FAKE_W, grid_slot=FAKE_W, seed=0, tokens_out=FAKE_W,
+                    frame_grid=None, n_slots=0, F_max=0, scores=FAKE_W, workspace=None)
+        for field in per_row:
+            a = mcd._step_args(**dict(base, **{field: None}))
+            a.workspace, a.workspace_bytes = 0x100000, 1 << 30
+            for f in (mcd._mcd_head_step, mcd._mcd_head_logits, mcd._mcd_sample_step):
+                assert f(h, ctypes.byref(a), None) == mcd.MCD_E_INVALID, (rk, field)
+                assert "per-row" in mcd.mcd_last_error()
+    mcd.mcd_head_destroy(h)
+
+
 def test_interleave_argument_errors():
     with pytest.raises(mcd.McdError):
         mcd._check(mcd._mcd_deinterleave(FAKE_W, 1, 2, 3, np.array([0, 1, 5], np.int32).ctypes.data,
@@ -148,13 +177,13 @@ def test_next_input_validation():
 
 
 def test_text_mask_validation():
-    h = _head(V_text=100, W_text=FAKE_W, T_text=64)
+    h = _text_head(T_text=64)
     mcd.mcd_head_destroy(h)
     for tt in (0, 100):
-        mcd.mcd_head_destroy(_head(V_text=100, W_text=FAKE_W, T_text=tt))
+        mcd.mcd_head_destroy(_text_head(T_text=tt))
     for tt in (-1, 50, 101, 96 + 32):
         with pytest.raises(mcd.McdError):
-            _head(V_text=100, W_text=FAKE_W, T_text=tt)
+            _text_head(T_text=tt)
 
 
 def test_phase_advance_matches_oracle():
