@@ -69,22 +69,26 @@ class TokenCheck:
         self.bad = []
 
     def add(self, gpu_tok, ora_tok, flags, rows=None, where=""):
-        rows = range(gpu_tok.shape[0]) if rows is None else rows
-        for r in rows:
-            for k in range(gpu_tok.shape[1]):
-                self.n += 1
-                g, o, f = int(gpu_tok[r, k]), int(ora_tok[r, k]), int(flags[r, k])
-                if g == o:
-                    continue
-                self.mismatch += 1
-                if f & oracle.FLAG_GAP_SMALL:
-                    self.exempt["gap"] += 1
-                elif f & oracle.FLAG_TOPP_EDGE:
-                    self.exempt["topp"] += 1
-                elif f & oracle.FLAG_TOPK_EDGE:
-                    self.exempt["topk"] += 1
-                else:
-                    self.bad.append((where, r, k, g, o, f))
+        g = np.asarray(gpu_tok)
+        o = np.asarray(ora_tok)
+        f = np.asarray(flags).astype(np.int64)
+        if rows is not None:
+            rows = np.asarray(list(rows))
+            g, o, f = g[rows], o[rows], f[rows]
+        else:
+            rows = np.arange(g.shape[0])
+        self.n += g.size
+        bad = g != o
+        self.mismatch += int(bad.sum())
+        gap = bad & ((f & oracle.FLAG_GAP_SMALL) > 0)
+        topp = bad & ~gap & ((f & oracle.FLAG_TOPP_EDGE) > 0)
+        topk = bad & ~gap & ~topp & ((f & oracle.FLAG_TOPK_EDGE) > 0)
+        self.exempt["gap"] += int(gap.sum())
+        self.exempt["topp"] += int(topp.sum())
+        self.exempt["topk"] += int(topk.sum())
+        for i, k in zip(*np.nonzero(bad & ~gap & ~topp & ~topk)):
+            self.bad.append((where, int(rows[i]), int(k), int(g[i, k]), int(o[i, k]),
+                             int(f[i, k])))
 
     def assert_ok(self, label=""):
         say(f"[{label}] positions={self.n} mismatches={self.mismatch} exempt={self.exempt} "

@@ -612,7 +612,7 @@ def test_unequal_streams_all_equal_is_the_equal_stream_head():
 
 
 # ---------------------------------------------------------------------------
-# Mixed-modality phases (Sec. 2.2): the text phase's vocabulary mask, modality
+# Mixed-modality phases (Sec. 2.3): the text phase's vocabulary mask, modality
 # inference from the unmasked distribution, and the phase state machine.
 
 def test_text_mask_and_modality_against_numpy_argmax():
@@ -673,3 +673,69 @@ def test_phase_machine_hand_traced():
     assert P.phase_advance(P.PHASE_TEXT, 0, 6, 1, [], end, 0) == (P.PHASE_AUDIO, 0, 6)
     assert P.phase_advance(P.PHASE_AUDIO, 4, 7, 0, [], end, 0) == (P.PHASE_TEXT, 0, -1)
     assert P.phase_advance(P.PHASE_TEXT, 0, 6, 1, [42], end, 0) == (P.PHASE_AUDIO, 0, 42)
+
+
+# ----------------------------------------------------------------------------
+# The sampler-alone checker: orc_sample_rows
+
+@pytest.mark.parametrize("case", ["topk_topp", "topp_only", "greedy_mixed", "unequal_streams"])
+def test_sample_rows_equals_head_step_on_its_scores(case):
+    """orc_sample_rows checks the GPU sampler when both sides are fed the same
+    scores, so its own row plumbing is pinned here against orc_head_step: fed
+    the fp64 scores head_step computed for the sampled rows, listed in a random
+    order with their companions, it must give the same tokens, gaps, flags and
+    frame-grid cells, copy each Main token to its companion, and leave every
+    other row untouched.  The rows carry different steps, temperatures, top-k,
+    top-p and request keys, so a row or score-offset mistake changes a token."""
+    kw = dict(H=32, K=4, V=67, n_pairs=5, n_solo=4, n_text=2, V_text=90, dtype="bf16",
+              steps=9, shuffle=True)
+    if case == "unequal_streams":
+        kw.update(V_stream=(67, 5, 31, 67), K=4)
+    wl = inputs.Workload("sr_" + case, **kw)
+    head = inputs.make_weights(wl)
+    lay = inputs.row_layout(wl)
+    rng = np.random.default_rng(11)
+    b = inputs.make_batch(wl, 0, lay)
+    R = wl.R
+    b["step"] = rng.integers(0, wl.steps, R).astype(np.int32)
+    b["temperature"] = rng.uniform(0.5, 1.5, R).astype(np.float32)
+    b["top_k"] = rng.integers(0, 12, R).astype(np.int32)
+    b["top_p"] = rng.uniform(0.5, 1.0, R).astype(np.float32)
+    b["rng_key"] = rng.integers(0, 2**63, R, dtype=np.uint64)
+    b["cfg_w"] = rng.uniform(1.0, 4.0, R).astype(np.float32)
+    if case == "topp_only":
+        b["top_k"][:] = 0
+    if case == "greedy_mixed":
+        b["temperature"][rng.random(R) < 0.5] = 0.0
+    F = wl.frames
+    g_ref = np.full((wl.n_slots, wl.K, F), -1, np.int32)
+    ref = oracle.head_step(head, b, seed=5, n_slots=wl.n_slots, F_max=F, frame_grid=g_ref)
+    kind = b["row_kind"]
+    sampled = [int(r) for r in np.where((kind == inputs.ROW_COND) | (kind == inputs.ROW_SOLO))[0]]
+    order = rng.permutation(len(sampled))
+    srow = [sampled[i] for i in order]
+    crow = [int(b["pair_map"][r]) if kind[r] == inputs.ROW_COND else -1 for r in srow]
+    scores = np.stack([ref["scores"][r] for r in srow])
+    g_got = np.full_like(g_ref, -1)
+    got = oracle.sample_rows(head, b, srow, crow, scores, seed=5, n_slots=wl.n_slots, F_max=F,
+                             frame_grid=g_got)
+    for r in range(R):
+        if kind[r] == inputs.ROW_TEXT:
+            assert (got["tokens"][r] == -1).all() and np.isinf(got["gap"][r]).all()
+            continue
+        assert np.array_equal(got["tokens"][r], ref["tokens"][r]), r
+        if kind[r] != inputs.ROW_UNCOND:
+            assert np.array_equal(got["gap"][r], ref["gap"][r]), r
+            assert np.array_equal(got["flags"][r], ref["flags"][r]), r
+    assert np.array_equal(g_got, g_ref)
+    # a companion left out (crow -1) keeps its untouched value
+    got2 = oracle.sample_rows(head, b, srow, [-1] * len(srow), scores, seed=5)
+    for r in np.where(kind == inputs.ROW_UNCOND)[0]:
+        assert (got2["tokens"][r] == -1).all()
+    # scores of two sampled rows exchanged: their results follow the scores only
+    # where the rows' own parameters agree, so at least one token must move
+    sw = scores.copy()
+    sw[[0, 1]] = sw[[1, 0]]
+    got3 = oracle.sample_rows(head, b, srow, crow, sw, seed=5)
+    assert not np.array_equal(got3["tokens"][srow[0]], ref["tokens"][srow[0]]) or \
+        not np.array_equal(got3["tokens"][srow[1]], ref["tokens"][srow[1]])
