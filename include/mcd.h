@@ -180,6 +180,26 @@ typedef struct {
  * `stream`); no device allocation, no synchronisation. */
 mcd_status mcd_head_step(const mcd_head *head, const mcd_step_args *args, hipStream_t stream);
 
+/* ---- allocation-free step ---------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc) and so
+ * cannot size mcd_head_step's workspace, whose text-head partials grow with
+ * the batch: the same step through the same kernels, with those partials in a
+ * device array the library holds per GPU (MCD_NOALLOC_SCRATCH_BYTES, from the
+ * first call on a device until the process ends).  Arguments as for
+ * mcd_head_step, except args->workspace: the status word region only
+ * (workspace_bytes >= 256, 256-byte aligned, zero-filled once; read it with
+ * mcd_read_device_status).  MCD_E_UNSUPPORTED, before anything is launched,
+ * when the text partials of the batch (n_text x ceil(V_text / 32) fp32 values
+ * and int32 ids, each block rounded up to 256 bytes) exceed the array: 220
+ * text rows at V_text = 151936.  No allocation, no synchronisation.  Every
+ * call on one GPU shares that GPU's array: calls that overlap in time on one
+ * GPU race.  A step's partials are written by its projection before its
+ * sampler reads them, so nothing carries over between calls. */
+#define MCD_NOALLOC_SCRATCH_BYTES (8u << 20)
+mcd_status mcd_head_step_noalloc(const mcd_head *head, const mcd_step_args *args,
+                                 hipStream_t stream);
+
 /* First half of a step: the K head projections of every audio row with the
  * CFG merge (Eq. 1) and temperature applied in the GEMM epilogue, written to
  * args->scores, and the text-head projection of the TEXT rows reduced to

@@ -54,6 +54,13 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 
+// Text-head partials kept outside the caller's workspace (the allocation-free
+// step): base address and capacity of that region; null: in the workspace.
+struct ExternalPartials {
+  char *base;
+  size_t cap;
+};
+
 // Bytes of the text partials of n text rows: the values, then the ids, each
 // rounded up to 256 bytes.
 size_t partials_bytes(const mcd_head *h, int64_t n) {
@@ -64,8 +71,10 @@ size_t partials_bytes(const mcd_head *h, int64_t n) {
 }
 
 // Shared validation of mcd_head_step / mcd_sample_step; fills the step view.
+// With ext, the workspace holds only the status word and the text partials go
+// to ext (which must hold them: checked by the caller).
 mcd_status make_step_view(const mcd_head *h, const mcd_step_args *a, bool need_hidden,
-                          mcd::StepView &sv) {
+                          mcd::StepView &sv, const ExternalPartials *ext = nullptr) {
   if (!h || !a) return fail(MCD_E_INVALID, "null head or args");
   const mcd::HeadView &hv = h->hv;
   const mcd_batch_counts &c = a->counts;
@@ -95,7 +104,7 @@ mcd_status make_step_view(const mcd_head *h, const mcd_step_args *a, bool need_h
   if (a->n_slots < 0 || a->F_max < 0) return fail(MCD_E_INVALID, "negative grid size");
   if (a->frame_grid && (int64_t)a->n_slots * hv.K * a->F_max > ((int64_t)1 << 40))
     return fail(MCD_E_INVALID, "frame grid too large");
-  const size_t need = mcd_workspace_bytes(h, a->R);
+  const size_t need = ext ? (size_t)mcd::kStatusBytes : mcd_workspace_bytes(h, a->R);
   if (!a->workspace || a->workspace_bytes < need)
     return fail(MCD_E_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 a->workspace ? a->workspace_bytes : (size_t)0);
@@ -132,9 +141,15 @@ mcd_status make_step_view(const mcd_head *h, const mcd_step_args *a, bool need_h
   sv.text_idx = nullptr;
   if (hv.V_text > 0) {
     const size_t parts = (size_t)sv.text_parts;
-    sv.text_val = reinterpret_cast<float *>(ws + mcd::kStatusBytes);
-    sv.text_idx = reinterpret_cast<int32_t *>(
-        ws + mcd::kStatusBytes + round_up((size_t)a->R * parts * sizeof(float), 256));
+    if (ext) {
+      sv.text_val = reinterpret_cast<float *>(ext->base);
+      sv.text_idx = reinterpret_cast<int32_t *>(
+          ext->base + round_up((size_t)c.n_text * parts * sizeof(float), 256));
+    } else {
+      sv.text_val = reinterpret_cast<float *>(ws + mcd::kStatusBytes);
+      sv.text_idx = reinterpret_cast<int32_t *>(
+          ws + mcd::kStatusBytes + round_up((size_t)a->R * parts * sizeof(float), 256));
+    }
   }
   return MCD_OK;
 }
@@ -149,6 +164,40 @@ bool make_delays(const int32_t *delays, int32_t K, mcd::Delays &d, int32_t &max_
     if (delays[k] > max_d) max_d = delays[k];
   }
   return true;
+}
+
+}  // namespace
+
+// ---- the allocation-free step's scratch ------------------------------------
+// One array per GPU, in the library's code object, held until the process
+// ends.  Host code never uses the array's name as an address (on the host it
+// is a stand-in for the device symbol): it takes the device address once per
+// device with hipGetSymbolAddress, with that device current, and passes that.
+constexpr size_t kScratchBytes = MCD_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array.
+mcd_status scratch_address(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "current device");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MCD_E_UNSUPPORTED, "device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "address of the scratch array");
+    if (!p) return fail(MCD_E_HIP, "address of the scratch array is null");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MCD_OK;
 }
 
 }  // namespace
@@ -344,6 +393,32 @@ hipError_t run_head_gemm(const mcd_head *h, const mcd::StepView &sv, hipStream_t
 mcd_status mcd_head_step(const mcd_head *h, const mcd_step_args *a, hipStream_t stream) {
   mcd::StepView sv;
   mcd_status s = make_step_view(h, a, true, sv);
+  if (s != MCD_OK) return s;
+  if (sv.R == 0) return MCD_OK;
+  hipError_t e = run_head_gemm(h, sv, stream);
+  if (e != hipSuccess) return hip_fail(e, "head GEMM launch");
+  e = mcd::launch_sample(h->hv, sv, true, stream);
+  if (e != hipSuccess) return hip_fail(e, "sample launch");
+  return MCD_OK;
+}
+
+mcd_status mcd_head_step_noalloc(const mcd_head *h, const mcd_step_args *a, hipStream_t stream) {
+  if (!h || !a) return fail(MCD_E_INVALID, "null head or args");
+  const int64_t n_text = a->counts.n_text;
+  const size_t need = partials_bytes(h, n_text);
+  if (need > kScratchBytes)
+    return fail(MCD_E_UNSUPPORTED,
+                "text partials of %lld rows need %zu bytes; the library's scratch holds %zu",
+                (long long)n_text, need, kScratchBytes);
+  ExternalPartials ext{nullptr, kScratchBytes};
+  if (need > 0) {
+    void *base = nullptr;
+    const mcd_status st = scratch_address(&base);
+    if (st != MCD_OK) return st;
+    ext.base = static_cast<char *>(base);
+  }
+  mcd::StepView sv;
+  mcd_status s = make_step_view(h, a, true, sv, &ext);
   if (s != MCD_OK) return s;
   if (sv.R == 0) return MCD_OK;
   hipError_t e = run_head_gemm(h, sv, stream);

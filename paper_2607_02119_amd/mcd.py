@@ -105,6 +105,8 @@ _mcd_workspace_bytes = _sig("mcd_workspace_bytes", ctypes.c_size_t, _vp, _i32)
 _mcd_head_step = _sig("mcd_head_step", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
 _mcd_sample_step = _sig("mcd_sample_step", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
 _mcd_head_logits = _sig("mcd_head_logits", ctypes.c_int, _vp, ctypes.POINTER(mcd_step_args), _vp)
+_mcd_head_step_noalloc = _sig("mcd_head_step_noalloc", ctypes.c_int, _vp,
+                              ctypes.POINTER(mcd_step_args), _vp)
 _mcd_deinterleave = _sig("mcd_deinterleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _vp, _vp)
 _mcd_interleave = _sig("mcd_interleave", ctypes.c_int, _vp, _i32, _i32, _i32, _vp, _i32, _vp, _vp)
 _mcd_next_input = _sig("mcd_next_input", ctypes.c_int, ctypes.POINTER(mcd_next_input_args), _vp)
@@ -117,6 +119,7 @@ _mcd_last_error = _sig("mcd_last_error", ctypes.c_char_p)
 
 EXPORTED = ["mcd_head_create", "mcd_head_destroy", "mcd_plan_words", "mcd_batch_plan",
             "mcd_plan_sampled_row", "mcd_workspace_bytes", "mcd_head_step", "mcd_head_logits",
+            "mcd_head_step_noalloc",
             "mcd_sample_step",
             "mcd_deinterleave", "mcd_interleave", "mcd_phase_advance", "mcd_next_input",
             "mcd_read_device_status",
@@ -220,6 +223,16 @@ def _step_args(R, counts, plan, hidden, cfg_w, temperature, top_k, top_p, rng_ke
 def mcd_head_step(h, stream=None, **kw):
     a = _step_args(**kw)
     _check(_mcd_head_step(h, ctypes.byref(a), _stream(stream)), "mcd_head_step")
+
+
+def mcd_head_step_noalloc(h, stream=None, **kw):
+    """mcd_head_step with the text-head partials in the library's per-GPU
+    array; `workspace` only needs the 256-byte status word region."""
+    a = _step_args(**kw)
+    _check(_mcd_head_step_noalloc(h, ctypes.byref(a), _stream(stream)), "mcd_head_step_noalloc")
+
+
+MCD_NOALLOC_SCRATCH_BYTES = 8 << 20
 
 
 def mcd_head_logits(h, stream=None, **kw):
