@@ -5,18 +5,22 @@
 A step is one pass of the whole hot path (mcd_head_step: head projections with
 the fused CFG merge and temperature, text-head argmax, selection, Gumbel-max
 draw, pads, companion copy, frame-grid scatter) over one batch of the workload.
-Inputs are resident in HBM before timing; the timed loop walks the workload's
-decode steps (each with its own hidden states and step index) and rotates
-through several copies of the weights so that they stream from HBM rather than
-from the 256 MB Infinity Cache.  The timed launches are issued one by one
-(--graphs captures them in HIP graphs beforehand and replays those instead;
-the step time came out the same and the weight-streaming projection read a
-few microseconds slower per launch, so replay is not the default).
+Inputs are resident in HBM before timing; the timed loop walks steady-state
+decode steps of the workload (every stream has a frame, so no step is cheapened
+by start-up or drain pads), each with its own hidden states and step index,
+and rotates through several copies of the weights so that they stream from HBM
+rather than from the 256 MB Infinity Cache.
 
-Prints one JSON line: value = client-visible codebook tokens per second
-(sampled rows x codebooks per step / step time), the roofline of the head
-projection kernel (the dominant one), and the CPU oracle timed on a bounded
-sample of the same workload.
+Prints one JSON line:
+  * value: client-visible codebook tokens per second of the headline workload
+    (weight_streaming: sampled rows x codebooks per step / step time);
+  * roofline: the head projection kernel (the dominant one), its time taken
+    in-step with HIP events between the projection and the sampler;
+  * legs: the same measurement on the MFMA-regime mixed batch and on the CFG
+    ablation (cfg_on / cfg_off, and their throughput ratio);
+  * cpu_baseline: the CPU oracle timed on a bounded sample of the headline
+    workload (one decode step), and parity: that sample's oracle tokens and
+    merged scores against the GPU's for the same step.
 """
 from __future__ import annotations
 
@@ -125,18 +129,43 @@ def copy_probe(torch):
     torch.cuda.empty_cache()
 
 
-def cpu_baseline(wl, budget_s=15.0):
-    """The CPU oracle (single-threaded, fp64) on a bounded sample of the workload:
-    whole Main/Companion pairs (or solo rows) of one decode step, added until
-    about budget_s seconds of CPU work.  Returns codebook tokens per second."""
+def host_cpu():
+    """The host's CPU model and the cores this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return model, os.cpu_count(), usable
+
+
+GAP_TOL, TOPK_TOL, TOPP_TOL = 1e-3, 1e-4, 1e-5   # the oracle's near-tie classes
+SCORE_TOL_BF16 = 1e-2
+
+
+def cpu_baseline(wl, t, gpu, budget_s=15.0):
+    """The CPU oracle (single-threaded, fp64) on a bounded sample of the
+    workload: whole Main/Companion pairs (or solo rows) of decode step t, added
+    until about budget_s seconds of CPU work.  Returns (baseline, parity): the
+    oracle's codebook tokens per second, and its tokens and merged scores for
+    those rows compared with the GPU's step t (gpu: tokens [R][K] and scores
+    [Rs][N] of the same step, plan_rows[s] = physical row of sampled index s)."""
     import oracle
     from paper_2607_02119_amd import inputs
 
-    t = wl.K + 1
     lay = inputs.row_layout(wl)
     head = inputs.make_weights(wl)
     b = inputs.make_batch(wl, t, lay)
     kinds = lay["row_kind"]
+    sampled_index = {r: s for s, r in enumerate(gpu["plan_rows"])}
     units = []   # lists of physical rows forming one sampled request
     for r in range(wl.R):
         if kinds[r] == inputs.ROW_COND:
@@ -144,6 +173,8 @@ def cpu_baseline(wl, budget_s=15.0):
         elif kinds[r] == inputs.ROW_SOLO:
             units.append([r])
     done_rows, tokens, elapsed = [], 0, 0.0
+    par = dict(positions=0, mismatches=0, exempt={"gap": 0, "topk": 0, "topp": 0},
+               unexplained=0, flagged={"gap": 0, "topk": 0, "topp": 0}, score_rel_err=0.0)
     for u in units:
         rows = u
         inv = {x: i for i, x in enumerate(rows)}
@@ -152,15 +183,50 @@ def cpu_baseline(wl, budget_s=15.0):
         sub["pair_map"] = np.array([inv[p] if p >= 0 else -1 for p in b["pair_map"][rows]],
                                    np.int32)
         t0 = time.perf_counter()
-        oracle.head_step(head, sub, seed=0, want_scores=False)
+        o = oracle.head_step(head, sub, seed=0, gap_tol=GAP_TOL, topk_tol=TOPK_TOL,
+                             topp_tol=TOPP_TOL)
         elapsed += time.perf_counter() - t0
         tokens += wl.K
         done_rows += rows
+        # parity of these rows against the GPU's step
+        g = gpu["tokens"][rows]
+        f = o["flags"].astype(np.int64)
+        bad = g != o["tokens"]
+        par["positions"] += int(g.size)
+        par["mismatches"] += int(bad.sum())
+        for name, bit in (("gap", oracle.FLAG_GAP_SMALL), ("topp", oracle.FLAG_TOPP_EDGE),
+                          ("topk", oracle.FLAG_TOPK_EDGE)):
+            par["flagged"][name] += int(((f & bit) > 0).sum())
+        gap = bad & ((f & oracle.FLAG_GAP_SMALL) > 0)
+        topp = bad & ~gap & ((f & oracle.FLAG_TOPP_EDGE) > 0)
+        topk = bad & ~gap & ~topp & ((f & oracle.FLAG_TOPK_EDGE) > 0)
+        par["exempt"]["gap"] += int(gap.sum())
+        par["exempt"]["topp"] += int(topp.sum())
+        par["exempt"]["topk"] += int(topk.sum())
+        par["unexplained"] += int((bad & ~gap & ~topp & ~topk).sum())
+        gs = gpu["scores"][sampled_index[rows[0]]].astype(np.float64)
+        os_ = o["scores"][0]
+        edges = np.concatenate([[0], np.cumsum(wl.stream_sizes)])
+        for k in range(wl.K):
+            gk, ok = gs[edges[k]:edges[k + 1]], os_[edges[k]:edges[k + 1]]
+            den = max(float(np.abs(ok).max()), 1e-300)
+            par["score_rel_err"] = max(par["score_rel_err"],
+                                       float(np.abs(gk - ok).max()) / den)
         if elapsed >= budget_s:
             break
-    return dict(value=tokens / elapsed, unit="codebook tokens/s", cores=1, kind="oracle",
+    model, n_cpu, usable = host_cpu()
+    base = dict(value=tokens / elapsed, unit="codebook tokens/s", cores=1, kind="oracle",
                 sample=f"decode step {t}: {len(done_rows)} of {wl.R} rows "
-                       f"({tokens} codebook tokens), {elapsed:.1f} s single-threaded fp64")
+                       f"({tokens} codebook tokens), {elapsed:.1f} s single-threaded fp64",
+                host_cpu=model, nproc=n_cpu, usable_cores=usable)
+    par.update(workload=wl.name, step=t, rows_checked=len(done_rows),
+               tolerances={"gap": GAP_TOL, "topk": TOPK_TOL, "topp": TOPP_TOL},
+               score_tol=SCORE_TOL_BF16 if wl.dtype == "bf16" else 1e-5,
+               score_rel_err=float(f"{par['score_rel_err']:.3e}"),
+               rule="tokens bit-exact except where the oracle's top-2 perturbed gap < 1e-3 "
+                    "(exempt.gap); exempt.topk / exempt.topp are mismatches at a top-k margin "
+                    "< 1e-4 or a top-p boundary within 1e-5, reported as departures")
+    return base, par
 
 
 # Stand-in backbone of the co-scheduling simulation: a memory-bound decoder
@@ -289,14 +355,189 @@ def cosched(args, torch):
         "cfg_on": on, "cfg_off": off}))
 
 
+class HipEvents:
+    """Timing events without the system-scope fence (hipEventDisableSystemFence):
+    a default event's fence writes back and invalidates the caches when it
+    completes, which costs microseconds and slows the kernel after it; these
+    only take the timestamps.  Created and read through the HIP runtime that
+    torch has loaded."""
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, n):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.c_void_p, ctypes.c_uint]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            rc = self.hip.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE)
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreateWithFlags: {rc}")
+            self.ev.append(e)
+
+    def record(self, i, stream):
+        rc = self.hip.hipEventRecord(self.ev[i], self.ct.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord: {rc}")
+
+    def ms(self, i, j):
+        out = self.ct.c_float()
+        rc = self.hip.hipEventElapsedTime(self.ct.byref(out), self.ev[i], self.ev[j])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime: {rc}")
+        return out.value
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(e)
+        self.ev = []
+
+
+class Leg:
+    """One workload resident on the GPU, timed over its steady-state decode
+    steps (every stream has a frame: no start-up or drain pads), each step with
+    its own hidden states and step index, rotating weight copies."""
+
+    def __init__(self, torch, wl, args, weights=None):
+        from paper_2607_02119_amd import harness
+
+        self.torch, self.wl, self.args = torch, wl, args
+        self.alg = algorithmic(wl)
+        self.copies = args.weight_copies or max(1, math.ceil(3 * MALL_BYTES /
+                                                             self.alg["weight_bytes"]))
+        self.dw = harness.DeviceWorkload(wl, weight_copies=self.copies, weights=weights)
+        live = wl.steps - 2 * wl.max_delay
+        self.n_hidden = max(1, min(live, args.steps + args.warmup, args.max_hidden_steps))
+        self.t0 = wl.max_delay
+        self.dw.load_hidden(range(self.t0, self.t0 + self.n_hidden))
+        self.stream = torch.cuda.current_stream()
+
+    def step_of(self, i):
+        return self.t0 + i % self.n_hidden, i % self.n_hidden, i % self.copies
+
+    def run(self, i, st):
+        t, h, c = self.step_of(i)
+        self.dw.run_step(t, hidden_index=h, copy=c, stream=st)
+
+    def logits(self, i, st):
+        t, h, c = self.step_of(i)
+        self.dw.run_logits(t, hidden_index=h, copy=c, stream=st)
+
+    def sample(self, i, st):
+        t, _, c = self.step_of(i)
+        self.dw.run_sample(t, copy=c, stream=st)
+
+    def measure(self, min_steps=0, min_warmup=0):
+        """Warm-up, then the timed loop of whole steps (value); then the
+        projection (mcd_head_logits) alone over the same steps, back to back:
+        its launch time, and the sampler's as the rest of the step; then the
+        steps again with a timing event after each of the two kernels (no cache
+        fence), reported beside them: each event adds command-processor time,
+        so that split is longer than the step.  All events are recorded on
+        the launch stream."""
+        torch, args = self.torch, self.args
+        warmup, steps = max(args.warmup, min_warmup), max(args.steps, min_steps)
+        for i in range(warmup):
+            self.run(i, self.stream)
+        torch.cuda.synchronize()
+        status = self.dw.status()
+        calls = [warmup + i for i in range(steps)]
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(self.stream)
+        for i in calls:
+            self.run(i, self.stream)
+        b.record(self.stream)
+        torch.cuda.synchronize()
+        ms_step = a.elapsed_time(b) / len(calls)
+        status |= self.dw.status()
+        # the projection alone, back to back over the same steps (device-bound:
+        # a launch takes far longer than the host needs to issue the next)
+        a.record(self.stream)
+        for i in calls:
+            self.logits(i, self.stream)
+        b.record(self.stream)
+        torch.cuda.synchronize()
+        self.ms_k1_loop = a.elapsed_time(b) / len(calls)
+        n = len(calls)
+        ev = HipEvents(2 * n + 1)
+        torch.cuda.synchronize()
+        ev.record(0, self.stream)
+        for j, i in enumerate(calls):
+            self.logits(i, self.stream)
+            ev.record(2 * j + 1, self.stream)
+            self.sample(i, self.stream)
+            ev.record(2 * j + 2, self.stream)
+        torch.cuda.synchronize()
+        k1 = float(np.mean([ev.ms(2 * j, 2 * j + 1) for j in range(n)]))
+        k2 = float(np.mean([ev.ms(2 * j + 1, 2 * j + 2) for j in range(n)]))
+        split_step = ev.ms(0, 2 * n) / n
+        ev.close()
+        status |= self.dw.status()
+        self.ms_step, self.ms_k1, self.ms_k2, self.ms_split = ms_step, k1, k2, split_step
+        self.status = status
+        return self
+
+    def summary(self):
+        wl, alg = self.wl, self.alg
+        t = self.ms_step * 1e-3
+        return {
+            "workload": wl.name, "rows": wl.R, "cfg_pairs": wl.n_pairs, "solo_rows": wl.n_solo,
+            "text_rows": wl.n_text, "K": wl.K, "V": wl.V, "V_text": wl.V_text,
+            "ms_per_step": round(self.ms_step, 5),
+            "codebook_tokens_per_s": round(wl.Rs * wl.K / t, 1),
+            "text_tokens_per_s": round(wl.n_text / t, 1),
+            "us_k1": round(self.ms_k1_loop * 1e3, 2),
+            "us_k2": round((self.ms_step - self.ms_k1_loop) * 1e3, 2),
+            "split_events": {"us_k1": round(self.ms_k1 * 1e3, 2),
+                             "us_k2": round(self.ms_k2 * 1e3, 2),
+                             "us_step": round(self.ms_split * 1e3, 2)},
+            "k1_mfma_frac": round(alg["flops"] / (self.ms_k1_loop * 1e-3) / 1e12 /
+                                  BF16_PEAK_TFLOPS, 4),
+            "k1_hbm_frac": round(alg["bytes"] / (self.ms_k1_loop * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "step_mfma_frac": round(alg["flops"] / t / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "step_hbm_frac": round(alg["bytes"] / t / 1e9 / HBM_PEAK_GBS, 4),
+            "weight_copies": self.copies, "device_status": self.status,
+        }
+
+    def free(self):
+        self.dw = None
+        self.torch.cuda.synchronize()
+        self.torch.cuda.empty_cache()
+
+
+def parity_step(leg):
+    """The whole batch at one steady-state step on the GPU (after the timed
+    loops), for the CPU oracle's comparison: tokens and merged scores."""
+    torch = leg.torch
+    t = leg.wl.K + 1
+    if not (leg.t0 <= t < leg.t0 + leg.n_hidden):
+        leg.dw.load_hidden([t])
+        hi = 0
+    else:
+        hi = t - leg.t0
+    leg.dw.tokens.fill_(-1)
+    leg.dw.run_step(t, hidden_index=hi, copy=0, stream=leg.stream)
+    torch.cuda.synchronize()
+    return t, dict(tokens=leg.dw.tokens.cpu().numpy(), scores=leg.dw.scores.cpu().numpy(),
+                   plan_rows=[r for r, _ in leg.dw.plan.sampled_rows()])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="weight_streaming")
-    ap.add_argument("--graphs", action="store_true",
-                    help="replay the timed launches from HIP graphs captured beforehand")
+    ap.add_argument("--max-hidden-steps", type=int, default=64,
+                    help="distinct decode steps (hidden states) the timed loop cycles through")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="time only the headline workload (not mfma_mixed, cfg_on, cfg_off)")
     ap.add_argument("--no-next-input", action="store_true",
                     help="skip the timing of the next-step input kernel")
     ap.add_argument("--weight-copies", type=int, default=0,
@@ -327,77 +568,24 @@ def main():
 
     from paper_2607_02119_amd import harness, inputs
 
-    wl = inputs.WORKLOADS[args.workload]
-    alg = algorithmic(wl)
-    copies = args.weight_copies or max(1, math.ceil(3 * MALL_BYTES / alg["weight_bytes"]))
+    def note(msg):
+        print(msg, file=sys.stderr, flush=True)
+
     torch.cuda.set_device(0)
     if args.copy_probe:
         copy_probe(torch)
-    dw = harness.DeviceWorkload(wl, weight_copies=copies)
-    n_hidden = min(wl.steps, args.steps + args.warmup)
-    dw.load_hidden(range(n_hidden))
-    stream = torch.cuda.current_stream()
-
-    def step(i):
-        t = i % n_hidden
-        dw.run_step(t, hidden_index=t, copy=i % copies, stream=stream)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    status = dw.status()
-
-    def timed(fn):
-        """Mean ms per call of fn(i), i = warmup .. warmup + steps - 1, back to
-        back on the launch stream between HIP events: issued one by one, or,
-        with --graphs, captured beforehand in HIP graphs of up to 50 calls each
-        and replayed once each (the same launches, without the host's
-        per-call cost)."""
-        calls = [args.warmup + i for i in range(args.steps)]
-        graphs = []
-        if args.graphs:
-            for c0 in range(0, len(calls), 50):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g):
-                    for i in calls[c0:c0 + 50]:
-                        fn(i, None)
-                graphs.append(g)
-            torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record(stream)
-        if not args.graphs:
-            for i in calls:
-                fn(i, stream)
-        else:
-            for g in graphs:
-                g.replay()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / len(calls)
-
-    def step_fn(i, st):
-        t = i % n_hidden
-        dw.run_step(t, hidden_index=t, copy=i % copies, stream=st)
-
-    # the whole step, then each of the two kernels alone over the same steps
-    def logits(i, st):
-        t = i % n_hidden
-        dw.run_logits(t, hidden_index=t, copy=i % copies, stream=st)
-
-    def sample(i, st):
-        dw.run_sample(i % n_hidden, copy=i % copies, stream=st)
-
-    ms_step = timed(step_fn)
-    status |= dw.status()
-    ms_k1 = timed(logits)
-    ms_k2 = timed(sample)
-    status |= dw.status()
+    wl = inputs.WORKLOADS[args.workload]
+    alg = algorithmic(wl)
+    leg = Leg(torch, wl, args).measure()
+    note(f"{wl.name}: {leg.ms_step * 1e3:.2f} us/step")
+    head = leg.summary()
+    status = leg.status
 
     # the next row of the path: the next-step input built from the last
     # step's tokens (sum of the K stream embeddings per row), timed alone
     next_input = None
     if not args.no_next_input:
+        dw = leg.dw
         dw.load_embeddings()
         # a different set of tokens per launch, so that the embedding rows
         # come from HBM as they do when each step's tokens are new
@@ -412,9 +600,33 @@ def main():
                       "us_per_launch": round(ms_ni * 1e3, 2), "algorithmic_bytes": ni_bytes,
                       "achieved": round(ni_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                       "frac": round(ni_gbs / HBM_PEAK_GBS, 4)}
+    par_t, par_gpu = parity_step(leg)
+    status |= leg.dw.status()
+    leg.free()
 
-    tokens_per_step = wl.Rs * wl.K
-    value = tokens_per_step / (ms_step * 1e-3)
+    # the other legs of the metric: the MFMA regime (mixed batch) and the CFG
+    # ablation (the same 512 rows as 256 CFG pairs and as 512 solo rows)
+    legs = {}
+    if not args.no_legs:
+        for name in ("mfma_mixed", "cfg_on", "cfg_off"):
+            other = inputs.WORKLOADS[name]
+            weights = legs.pop("_cfg_weights", None) if name == "cfg_off" else None
+            lg = Leg(torch, other, args, weights=weights).measure(min_steps=100, min_warmup=20)
+            note(f"{name}: {lg.ms_step * 1e3:.2f} us/step")
+            legs[name] = lg.summary()
+            if name == "cfg_on":
+                legs["_cfg_weights"] = lg.dw.host_head
+            lg.free()
+        legs.pop("_cfg_weights", None)
+        on, off = legs["cfg_on"], legs["cfg_off"]
+        legs["cfg_ratio"] = {
+            "client_tokens": round(on["codebook_tokens_per_s"] / off["codebook_tokens_per_s"], 4),
+            "rows_processed": round(off["ms_per_step"] / on["ms_per_step"], 4),
+            "paper_context": "0.80: whole-system decode tok/s with / without CFG, Bagpiper on "
+                             "vLLM, 1x H100 80 GB (Table 4); a context figure, not a target"}
+
+    value = wl.Rs * wl.K / (leg.ms_step * 1e-3)
+    ms_k1 = leg.ms_k1_loop
     mfma_bound = alg["flops"] / (BF16_PEAK_TFLOPS * 1e12) > alg["bytes"] / (HBM_PEAK_GBS * 1e9)
     if mfma_bound:
         ach = alg["flops"] / (ms_k1 * 1e-3) / 1e12
@@ -426,6 +638,9 @@ def main():
                     frac=round(ach / HBM_PEAK_GBS, 4))
     roof.update(traffic=k1_traffic(wl.name), kernel="head_gemm (mcd_head_logits)",
                 us_per_launch=round(ms_k1 * 1e3, 2),
+                measured="HIP events around back-to-back projection launches over the "
+                         "timed steps (in-step events add command-processor time per "
+                         "event: step.split_events)",
                 algorithmic_bytes=alg["bytes"], algorithmic_flops=alg["flops"])
     out = {
         "metric": "codebook tokens/sec per CFG-paired decode step",
@@ -434,7 +649,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
+        "ms_per_step": round(leg.ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -444,17 +659,21 @@ def main():
                    "solo_rows": wl.n_solo, "text_rows": wl.n_text, "H": wl.H, "K": wl.K,
                    "V": wl.V, "V_text": wl.V_text, "cfg_w": wl.cfg_w,
                    "temperature": wl.temperature, "top_k": wl.top_k, "top_p": wl.top_p,
-                   "weight_copies": copies, "parallelism": "single GPU"},
+                   "weight_copies": leg.copies, "decode_steps": f"{leg.t0}..{leg.t0 + leg.n_hidden - 1}",
+                   "parallelism": "single GPU"},
         "roofline": roof,
-        "step": {"hbm_frac": round(alg["bytes"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                 "mfma_frac": round(alg["flops"] / (ms_step * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                 "us_sample_kernel": round(ms_k2 * 1e3, 2),
-                 "device_status": status},
+        "step": {"hbm_frac": head["step_hbm_frac"], "mfma_frac": head["step_mfma_frac"],
+                 "us_k1": head["us_k1"], "us_k2": head["us_k2"],
+                 "split_events": head["split_events"], "device_status": status},
     }
+    if legs:
+        out["legs"] = legs
     if next_input is not None:
         out["next_input"] = next_input
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+        base, par = cpu_baseline(wl, par_t, par_gpu, args.cpu_budget)
+        out["cpu_baseline"] = base
+        out["parity"] = par
     print(json.dumps(out), flush=True)
 
 
