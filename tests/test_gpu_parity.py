@@ -177,6 +177,23 @@ RAGGED = [
                                      shuffle=True)),
     ("mfma_text_rows", dict(H=128, K=2, V=40, n_pairs=3, n_solo=2, n_text=150, V_text=300,
                             dtype="bf16", top_k=5, steps=3, shuffle=True)),
+    # streaming tiles that never straddle two streams (V a multiple of the
+    # 64-, 128- and 256-column tile widths), every draw path; a small p so that
+    # the first candidate often falls outside the nucleus
+    ("aligned_topp_bn64", dict(H=256, K=3, V=256, n_pairs=20, n_solo=7, dtype="bf16", top_p=0.9,
+                            cfg_w=2.5, steps=6, shuffle=True)),
+    ("aligned_small_p", dict(H=128, K=4, V=512, n_pairs=9, n_solo=6, dtype="bf16", top_p=0.3,
+                          temperature=0.7, steps=7, shuffle=True)),
+    ("aligned_plain_sampling", dict(H=64, K=2, V=1024, n_pairs=5, n_solo=3, dtype="bf16",
+                                 steps=4)),
+    ("aligned_topk_text", dict(H=128, K=4, V=512, n_pairs=10, n_solo=5, n_text=6, V_text=700,
+                            dtype="bf16", top_k=20, steps=6, shuffle=True)),
+    ("aligned_bn128", dict(H=128, K=8, V=4096, n_pairs=3, n_solo=2, dtype="bf16", top_p=0.95,
+                        cfg_w=2.0, steps=10)),
+    ("aligned_bn256", dict(H=64, K=16, V=4096, n_pairs=4, n_solo=1, dtype="bf16", top_p=0.9,
+                        steps=17)),
+    ("aligned_greedy", dict(H=64, K=3, V=128, n_pairs=4, n_solo=3, dtype="bf16", temperature=0.0,
+                         steps=5)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
                               dtype="f32", top_k=5, top_p=0.8, steps=5, shuffle=True)),
     ("bf16_greedy", dict(H=64, K=4, V=100, n_pairs=5, n_solo=4, dtype="bf16", temperature=0.0,
@@ -480,3 +497,50 @@ def test_corrupt_plan_header_gives_pad_tokens_and_flag():
     torch.cuda.synchronize()
     assert dw.status() == 0
     assert np.array_equal(_cpu(dw.tokens), good)
+
+
+MIXED_ROW_SHAPES = [
+    dict(H=256, K=3, V=256, n_pairs=20, n_solo=7, shuffle=True),
+    dict(H=128, K=8, V=4096, n_pairs=60, n_solo=8),
+    dict(H=64, K=16, V=4096, n_pairs=4, n_solo=1),
+]
+
+
+@pytest.mark.parametrize("shape", range(len(MIXED_ROW_SHAPES)))
+def test_rows_with_every_draw_path_in_one_batch(shape):
+    """Every draw path in one batch, row by row: greedy, top-k, top-p with a
+    small and a large p, plain sampling, and top-k with top-p.  mcd_head_step
+    and mcd_head_logits followed by mcd_sample_step give the same tokens bit
+    for bit, and they agree with the oracle."""
+    kw = MIXED_ROW_SHAPES[shape]
+    wl = inputs.Workload(f"mixed_rows_{shape}", dtype="bf16", steps=kw["K"] + 3, **kw)
+    say(f"case every draw path {kw}")
+    dw = harness.DeviceWorkload(wl)
+    t = wl.K + 1
+    dw.load_hidden([t])
+    rng = np.random.default_rng(shape)
+    R = wl.R
+    T = rng.choice([0.0, 0.7, 1.0, 1.3], R).astype(np.float32)
+    top_k = rng.choice([0, 0, 5, 50, wl.V], R).astype(np.int32)
+    top_p = rng.choice([1.0, 0.95, 0.5, 0.2], R).astype(np.float32)
+    for name, val in (("temperature", T), ("top_k", top_k), ("top_p", top_p)):
+        dw.params[name].copy_(torch.from_numpy(val))
+    outs = []
+    for mode in ("step", "split"):
+        dw.tokens.fill_(-1)
+        if mode == "step":
+            dw.run_step(t, hidden_index=0)
+        else:
+            dw.run_logits(t, hidden_index=0)
+            dw.run_sample(t)
+        torch.cuda.synchronize()
+        outs.append(_cpu(dw.tokens).copy())
+    assert np.array_equal(outs[0], outs[1])
+    b = inputs.make_batch(wl, t, dw.layout)
+    b.update(temperature=T, top_k=top_k, top_p=top_p)
+    o = oracle.head_step(dw.host_head, b, seed=dw.seed, gap_tol=GAP_TOL, topk_tol=TOPK_TOL,
+                         topp_tol=TOPP_TOL)
+    tc = TokenCheck()
+    tc.add(outs[0], o["tokens"], o["flags"], where=f"t={t}")
+    tc.assert_ok(f"every draw path {shape}")
+    assert dw.status() == 0
