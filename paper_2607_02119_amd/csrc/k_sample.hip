@@ -195,7 +195,7 @@ struct Smem {
     int id;
     unsigned long long m;                // mass (top-p)
   };
-  static constexpr int kDraw = 4 * TPV;  // every group of four ids of a vector
+  static constexpr int kDraw = TPV;      // kept groups dealt through the list (one per thread)
   uint32_t cnt[kBins + 1];               // top-k bin counts
   union {
     unsigned long long mh[kBins + 1];    // top-p bin masses (the last: the open bin)
@@ -1126,27 +1126,39 @@ __device__ __forceinline__ int select_and_draw(const StepView &sv, const float (
     for (int j = 0; j < 4; ++j)
       if ((bits >> j) & 1) keep_better(bv, bi, xs[j] + gumbel_from_word(w.w[j]), 4 * g + j);
   };
-  // The groups with kept ids move to an LDS list and are dealt to the threads
-  // in turn, so that the threads run the same number of Philox blocks, up to one.
-  static_assert(GPT * TPV <= Smem<TPV>::kDraw, "the draw list holds every group");
+  // When there are at most as many groups with kept ids as threads (top-k
+  // cuts of up to TPV ids always), they move to an LDS list and each thread
+  // draws one, so that no thread runs several Philox blocks while others
+  // idle.  More groups (a wide top-k or top-p set) are drawn by their owner
+  // threads: as many blocks per thread as kept groups it holds.  A list of one
+  // entry per thread keeps the sampler's LDS small enough for eight
+  // workgroups per compute unit.
   uint32_t n = 0;
 #pragma unroll
   for (int q = 0; q < GPT; ++q) n += ((kept >> (4 * q)) & 0xFu) ? 1u : 0u;
   uint32_t total;
   uint32_t pos = grp_excl_scan_u32<TPV>(n, total, sm, slot);
-  // the list shares its storage with the histograms and radix buffers: their
-  // last readers are past the scan (or, in one wave, earlier in program order)
-  if constexpr (TPV == kWave) Grp<TPV>::sync();
-  DrawItem *dl = sm.u.draw;
+  if (total <= (uint32_t)Smem<TPV>::kDraw) {   // group-uniform
+    // the list shares its storage with the histograms and radix buffers: their
+    // last readers are past the scan (or, in one wave, earlier in program order)
+    if constexpr (TPV == kWave) Grp<TPV>::sync();
+    DrawItem *dl = sm.u.draw;
 #pragma unroll
-  for (int q = 0; q < GPT; ++q) {
-    const uint32_t bits = (kept >> (4 * q)) & 0xFu;
-    if (bits) dl[pos++] = {q * TPV + gt, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
-  }
-  Grp<TPV>::sync();
-  for (int e = gt; e < (int)total; e += TPV) {
-    const DrawItem it = dl[e];
-    draw(it.g, it.bits, it.x[0], it.x[1], it.x[2], it.x[3]);
+    for (int q = 0; q < GPT; ++q) {
+      const uint32_t bits = (kept >> (4 * q)) & 0xFu;
+      if (bits) dl[pos++] = {q * TPV + gt, bits, {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]}};
+    }
+    Grp<TPV>::sync();
+    if (gt < (int)total) {
+      const DrawItem it = dl[gt];
+      draw(it.g, it.bits, it.x[0], it.x[1], it.x[2], it.x[3]);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < GPT; ++q) {
+      const uint32_t bits = (kept >> (4 * q)) & 0xFu;
+      if (bits) draw(q * TPV + gt, bits, x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
+    }
   }
   return grp_argmax_f32<TPV>(bv, bi, sm, slot);
 }

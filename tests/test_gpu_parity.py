@@ -194,6 +194,8 @@ RAGGED = [
                         steps=17)),
     ("aligned_greedy", dict(H=64, K=3, V=128, n_pairs=4, n_solo=3, dtype="bf16", temperature=0.0,
                          steps=5)),
+    ("wide_topk_owner_draw", dict(H=128, K=3, V=2048, n_pairs=5, n_solo=3, dtype="bf16",
+                                  top_k=1000, steps=5, shuffle=True)),
     ("f32_ragged_mixed", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=2, V_text=70,
                               dtype="f32", top_k=5, top_p=0.8, steps=5, shuffle=True)),
     ("bf16_greedy", dict(H=64, K=4, V=100, n_pairs=5, n_solo=4, dtype="bf16", temperature=0.0,
@@ -269,6 +271,11 @@ SAMPLER = [
     (256, 4, 256, 2.0, 0.0, 0.0, 0, 1.0),        # greedy
     (256, 4, 256, 1.0, 0.25, 1.0, 0, 0.3),       # no top-k cut, small p, heavy ties
     (1000, 4, 256, 0.0, 0.0, 1.0, 0, 0.5),       # no top-k cut, all scores equal
+    # more groups of kept ids than threads per vector: drawn by their owners
+    (4096, 2, 4, 2.0, 0.0, 1.0, 1500, 1.0),      # workgroup per vector
+    (4096, 2, 4, 2.0, 0.0, 1.0, 1500, 0.9),      # and top-p over the survivors
+    (1024, 16, 64, 3.6, 0.0, 0.8, 300, 1.0),     # one wave per vector
+    (1024, 16, 64, 1.0, 0.25, 1.0, 700, 0.95),   # heavy ties
 ]
 
 
