@@ -437,9 +437,9 @@ class Leg:
         projection (mcd_head_logits) alone over the same steps, back to back:
         its launch time, and the sampler's as the rest of the step; then the
         steps again with a timing event after each of the two kernels (no cache
-        fence), reported beside them: each event adds command-processor time,
-        so that split is longer than the step.  All events are recorded on
-        the launch stream."""
+        fence), reported beside them: on some machines each event adds
+        command-processor time, so that split can be longer than the step.
+        All events are recorded on the launch stream."""
         torch, args = self.torch, self.args
         warmup, steps = max(args.warmup, min_warmup), max(args.steps, min_steps)
         for i in range(warmup):
