@@ -54,8 +54,8 @@ MEASURED_TRAFFIC = {
     # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
     "weight_streaming": dict(
         sources=["k_stream.hip", "stream_tile.h", "gemm_common.h"],
-        sha256="f026eec05ce4811440c25fa305ca150d277aa4042f56379e7b223732309f1849",
-        fetch_bytes=277193114, write_bytes=8388608,
+        sha256="0ff8493d7b7cd6d9b33aa6e65e15a01c4a5ccdf80d95108b26bb87f4eb46e34e",
+        fetch_bytes=277192704, write_bytes=8388608,
         profile="profiles/head_step_weight_streaming.md"),
 }
 

@@ -1,12 +1,14 @@
 // K1, MFMA-regime path (more than 128 GEMM rows): the same projection and
 // fused epilogues as the streaming path (Sec. 2.1, Eq. 1), for batches whose
-// arithmetic intensity puts them on the matrix cores.
+// arithmetic intensity puts them on the matrix cores: audio rows in 256 x 256
+// tiles when those fill the chip (other audio batches take the streaming
+// path's 128 x 256 tiles), text rows beyond 128 in 256 x 128 tiles.
 #include "mfma2_tile.h"
 
 namespace mcd {
 namespace {
 
-// MFMA-regime path for more than 128 GEMM rows (bf16, H a multiple of 32).
+// 256 x 128 tiles for more than 128 text rows (bf16, H a multiple of 32).
 // A workgroup owns a 256 x 128 output tile with eight waves, two per SIMD, so
 // that one wave's MFMAs cover the other's LDS reads and copies.  The waves
 // split it by row half (wm = wave & 1), column half (wn = (wave >> 1) & 1) and
@@ -282,9 +284,10 @@ hipError_t launch_mfma(const HeadView &hv, const StepView &sv, int M, int N, hip
 
 hipError_t launch_mfma_gemm(const HeadView &hv, const StepView &sv, bool text, hipStream_t st) {
   if (text) return launch_mfma<true>(hv, sv, sv.n_text, hv.V_text, st);
-  // 256 x 256 tiles when they fill the chip, else 256 x 128
+  // 256 x 256 tiles when they fill the chip, else the streaming path's
+  // 128 x 256 tiles
   if (tiles_256(sv.Mg, hv.N) >= 256) return launch_mfma2(hv, sv, st);
-  return launch_mfma<false>(hv, sv, sv.Mg, hv.N, st);
+  return launch_stream_rows(hv, sv, st);
 }
 
 }  // namespace mcd

@@ -1,4 +1,6 @@
-// K1, weight-streaming path (at most 128 GEMM rows): codebook-head projection
+// K1, weight-streaming path (at most 128 GEMM rows; also audio batches of
+// more than 128 rows that do not fill the chip with 256 x 256 tiles, in
+// 128-row tiles): codebook-head projection
 // with the CFG merge and temperature fused into the epilogue, or the text-head
 // projection with a fused (max, lowest argmax) epilogue.
 //
@@ -46,6 +48,14 @@ hipError_t launch_skinny(const HeadView &hv, const StepView &sv, int M, int N, h
 }
 
 }  // namespace
+
+// Audio batches of more than 128 GEMM rows that make fewer than 256 tiles of
+// 256 x 256 (the cfg workloads' 512 rows): 128 x 256 tiles, row tile by row
+// tile.  Their 64-k slices read whole 128-byte row segments; the 256 x 128
+// MFMA tiles' 32-k slices read half segments and took 5-12 % longer.
+hipError_t launch_stream_rows(const HeadView &hv, const StepView &sv, hipStream_t st) {
+  return launch_dma<128, 256, false>(hv, sv, sv.Mg, hv.N, st);
+}
 
 hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
                               hipStream_t st) {

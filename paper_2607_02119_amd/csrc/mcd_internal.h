@@ -76,6 +76,8 @@ hipError_t launch_head_gemm(const HeadView &hv, const StepView &sv, hipStream_t 
 hipError_t launch_head_gemm_part(const HeadView &hv, const StepView &sv, bool text,
                                  hipStream_t stream);
 // bf16 projection kernels (audio rows, or the text rows when text is set)
+hipError_t launch_stream_rows(const HeadView &hv, const StepView &sv,
+                              hipStream_t st);       // audio rows in 128 x 256 tiles
 hipError_t launch_stream_gemm(const HeadView &hv, const StepView &sv, bool text,
                               hipStream_t stream);   // at most 128 GEMM rows
 hipError_t launch_mfma_gemm(const HeadView &hv, const StepView &sv, bool text,

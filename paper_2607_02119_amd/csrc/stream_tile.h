@@ -1,4 +1,4 @@
-// Tile body of the K1 weight-streaming path (at most 128 GEMM rows):
+// Tile body of the K1 weight-streaming path (at most 128 GEMM rows per tile):
 // codebook-head projection with the CFG merge and temperature fused into the
 // epilogue, or the text-head projection with a fused (max, lowest argmax)
 // epilogue.
@@ -15,8 +15,8 @@
 namespace mcd {
 namespace {
 
-// Weight-streaming path for up to 128 rows.  A workgroup owns all BM rows and
-// BN columns.  Each k slice of SK = 64 (128 bytes of every weight and hidden
+// Weight-streaming path, tiles of up to 128 rows.  A workgroup owns BM rows
+// (all of them when there are at most 128) and BN columns.  Each k slice of SK = 64 (128 bytes of every weight and hidden
 // row) goes into one of the LDS stages of its ring.  Waves 0-1 copy weight
 // slices with global_load_lds_dwordx4 (64 lanes x 16 B, eight 128-byte row
 // segments per instruction, no registers), SW - 1 slices ahead of their use.
@@ -118,6 +118,15 @@ __device__ __forceinline__ void dma_tile(const HeadView &hv, const StepView &sv,
   const int NST = H / SK;
 
   const int tiles_m = (M + BM - 1) / BM;
+  // Several row tiles (more than 128 audio rows): workgroups are dealt to the
+  // 8 XCDs in turn, so the index is remapped to give each XCD a contiguous
+  // run of tiles, in which the row tiles of a column tile are neighbours, run
+  // at the same time and walk k in the same order: they share that column
+  // tile's weights through the XCD's L2.
+  if (tiles_m > 1) {
+    const int ntiles = tiles_m * ((N + BN - 1) / BN);
+    if (ntiles % 8 == 0) bx = (bx % 8) * (ntiles / 8) + bx / 8;
+  }
   const int tile_m = bx % tiles_m;
   const int tile_n = bx / tiles_m;
   const int m0 = tile_m * BM, n0 = tile_n * BN;

@@ -116,7 +116,7 @@ RAGGED = [
                               bias=True)),
     ("bias_stream_wide", dict(H=128, K=9, V=3739, n_pairs=20, n_solo=3, dtype="bf16", top_k=20,
                               steps=10, bias=True)),
-    ("bias_mfma", dict(H=192, K=4, V=256, n_pairs=100, n_solo=100, dtype="bf16", top_p=0.9,
+    ("bias_rows", dict(H=192, K=4, V=256, n_pairs=100, n_solo=100, dtype="bf16", top_p=0.9,
                        cfg_w=2.5, steps=4, bias=True)),
     ("bias_fused_mixed", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, n_text=70, V_text=900,
                               dtype="bf16", top_k=15, steps=10, shuffle=True, bias=True)),
@@ -132,12 +132,12 @@ RAGGED = [
     ("stream_wide_bm128", dict(H=192, K=9, V=3700, n_pairs=60, n_solo=5, n_text=100,
                                V_text=40000, dtype="bf16", top_p=0.9, cfg_w=2.5, steps=10)),
     # streams of unequal size (one large stream and smaller ones): the
-    # streaming kernel with N % 4 != 0, the 256 x 128 MFMA kernel, and the
+    # streaming kernel with N % 4 != 0, 128-row streaming tiles, and the
     # one-wave-per-vector sampler
     ("unequal_streams_stream", dict(H=128, K=4, V=100, V_stream=(100, 37, 64, 5), n_pairs=6,
                                     n_solo=2, n_text=2, V_text=300, dtype="bf16", top_k=7,
                                     temperature=0.8, steps=6, shuffle=True, bias=True)),
-    ("unequal_streams_mfma", dict(H=64, K=9, V=2048, V_stream=(2048,) + (1024,) * 8,
+    ("unequal_streams_rows", dict(H=64, K=9, V=2048, V_stream=(2048,) + (1024,) * 8,
                                   n_pairs=100, n_solo=60, dtype="bf16", top_p=0.9, cfg_w=2.5,
                                   steps=10)),
     ("unequal_streams_wave", dict(H=64, K=8, V=1000, V_stream=(1000, 500, 250, 125, 1000, 999, 3, 64),
@@ -155,17 +155,21 @@ RAGGED = [
                              T_text=64, dtype="bf16", top_k=15, steps=9, shuffle=True)),
     ("text_mask_f32", dict(H=40, K=3, V=37, n_pairs=3, n_solo=2, n_text=4, V_text=70,
                            T_text=32, dtype="f32", top_k=5, steps=4, shuffle=True)),
-    # more than 128 GEMM rows: the MFMA-regime kernel (256 x 128 tiles)
-    ("mfma_two_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
+    # more than 128 audio rows and fewer than 256 tiles of 256 x 256: 128 x 256
+    # streaming tiles, row tile by row tile (here three, the last one ragged)
+    ("rows_three_row_tiles", dict(H=128, K=3, V=100, n_pairs=150, n_solo=7, dtype="bf16", top_k=10,
                                 temperature=0.9, steps=4, shuffle=True)),
-    # 2 x 8 tiles of 256 x 128: the XCD-aware order
-    ("mfma_xcd_remap", dict(H=192, K=4, V=256, n_pairs=100, n_solo=100, dtype="bf16", top_p=0.9,
+    # 2 x 4 and 3 x 8 tiles of 128 x 256 (the second with a ragged row tile):
+    # the XCD-aware order
+    ("rows_xcd_remap", dict(H=192, K=4, V=256, n_pairs=100, n_solo=56, dtype="bf16", top_p=0.9,
                             cfg_w=2.5, steps=4)),
+    ("rows_xcd_remap_ragged", dict(H=256, K=4, V=512, n_pairs=140, n_solo=20, dtype="bf16",
+                                   top_k=30, temperature=0.9, steps=5, shuffle=True)),
     # at least 256 tiles of 256 x 256: the wide-tile kernel, ragged N and V % 4 != 0
     ("mfma_wide_tiles", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, dtype="bf16",
                              top_k=15, temperature=0.8, steps=10, shuffle=True)),
-    # 2 x 128 tiles of 256 x 128 with a ragged last column tile (V % 4 != 0)
-    ("mfma_ragged_columns", dict(H=256, K=4, V=4093, n_pairs=140, n_solo=20, dtype="bf16",
+    # 3 x 64 tiles of 128 x 256 with a ragged last row and column tile (V % 4 != 0)
+    ("rows_ragged_columns", dict(H=256, K=4, V=4093, n_pairs=140, n_solo=20, dtype="bf16",
                                  top_k=10, temperature=0.9, steps=3, shuffle=True)),
     # one launch for both projections: 256 tiles of 256 x 256 for the audio
     # rows, then 65..128 text rows in 256-column (or 64-column) streaming tiles
