@@ -24,6 +24,10 @@ CASES = [
     # audio and text rows on two streams (fork and join inside the graph)
     ("graph_two_streams", dict(H=128, K=3, V=37, n_pairs=10, n_solo=5, n_text=3, V_text=300,
                                dtype="bf16", top_k=7, steps=6, shuffle=True)),
+    # more than 128 audio rows below 256 tiles of 256 x 256: 128 x 256
+    # streaming row tiles in the XCD-aware order (3 x 8 tiles)
+    ("graph_row_tiles", dict(H=256, K=4, V=512, n_pairs=140, n_solo=20, dtype="bf16", top_k=20,
+                             steps=6, shuffle=True)),
     # the single mixed launch (256 tiles of 256 x 256 and 70 text rows)
     ("graph_fused_mixed", dict(H=64, K=8, V=4093, n_pairs=100, n_solo=60, n_text=70,
                                V_text=900, dtype="bf16", top_k=15, steps=9, shuffle=True)),
