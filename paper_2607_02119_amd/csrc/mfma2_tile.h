@@ -21,7 +21,8 @@ inline int64_t tiles_256(int32_t M, int32_t N) {
 // of weights (waves 0-1 copy weights, waves 2-3 hidden states, 8 copies each)
 // for 4 x 32 MFMAs: a third fewer bytes per MFMA than a 256 x 128 tile, and
 // half the fragment reads.  All four ring stages are in flight.  It needs at
-// least 256 tiles to fill the chip; smaller batches use the 256 x 128 kernel.
+// least 256 tiles to fill the chip; smaller batches take the streaming path's
+// 128 x 256 row tiles.
 
 // LDS of one tile: the rings (or, after the loop, one 128-row half of the
 // epilogue tile) and the row-pair parameters after them.
