@@ -54,8 +54,8 @@ MEASURED_TRAFFIC = {
     # workload: dict(sources=[...], sha256=..., fetch_bytes=..., write_bytes=..., profile=...)
     "weight_streaming": dict(
         sources=["k_stream.hip", "stream_tile.h", "gemm_common.h"],
-        sha256="0ff8493d7b7cd6d9b33aa6e65e15a01c4a5ccdf80d95108b26bb87f4eb46e34e",
-        fetch_bytes=277192704, write_bytes=8388608,
+        sha256="94f40a0df98a9499182f4752cf032ebceebce6b0cc4b38870b52a7302311baa4",
+        fetch_bytes=277193728, write_bytes=8388608,
         profile="profiles/head_step_weight_streaming.md"),
 }
 

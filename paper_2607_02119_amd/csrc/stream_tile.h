@@ -284,23 +284,38 @@ __device__ __forceinline__ void dma_tile(const HeadView &hv, const StepView &sv,
     }
   }
 
-  // MFMAs of slice st, from its stages
-  auto compute = [&](int st) __attribute__((always_inline)) {
+  // MFMAs of slice st, from its stages.  The fragments of the next k16 step
+  // are read while the MFMAs of this one run, and extra(m) (this wave's copy
+  // work for a later slice) is issued after MFMA m, so that the matrix pipe,
+  // the LDS and the load path work at once instead of in turn.
+  constexpr int NMF = KS * MB * NB;        // MFMAs per wave and slice
+  auto compute = [&](int st, auto &&extra) __attribute__((always_inline)) {
     const char *wsb = wring + (st % SW) * WST;
     const char *asb = aring + (st % SA) * AST;
-#pragma unroll
-    for (int s2 = 0; s2 < KS; ++s2) {
-      bf16x8 a[MB], b[NB];
-#pragma unroll
-      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const bf16x8 *>(asb + aoff[s2][i]);
-#pragma unroll
-      for (int j = 0; j < NB; ++j) b[j] = *reinterpret_cast<const bf16x8 *>(wsb + woff[s2][j]);
-#pragma unroll
-      for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
+    bf16x8 fa[2][MB], fb[2][NB];
+    static_for<0, MB>([&](auto ic) __attribute__((always_inline)) {
+      fa[0][ic] = *reinterpret_cast<const bf16x8 *>(asb + aoff[0][ic]);
+    });
+    static_for<0, NB>([&](auto jc) __attribute__((always_inline)) {
+      fb[0][jc] = *reinterpret_cast<const bf16x8 *>(wsb + woff[0][jc]);
+    });
+    static_for<0, KS>([&](auto sc) __attribute__((always_inline)) {
+      constexpr int s2 = decltype(sc)::value, cur = s2 & 1, nxt = cur ^ 1;
+      if constexpr (s2 + 1 < KS) {
+        static_for<0, MB>([&](auto ic) __attribute__((always_inline)) {
+          fa[nxt][ic] = *reinterpret_cast<const bf16x8 *>(asb + aoff[s2 + 1][ic]);
+        });
+        static_for<0, NB>([&](auto jc) __attribute__((always_inline)) {
+          fb[nxt][jc] = *reinterpret_cast<const bf16x8 *>(wsb + woff[s2 + 1][jc]);
+        });
+      }
+      static_for<0, MB * NB>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value, i = m / NB, j = m % NB;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+        extra(std::integral_constant<int, s2 * MB * NB + m>{});
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
   };
   // The two roles run separate copies of the loop (one barrier per iteration
   // in both), so that the hidden-state registers exist on one path only.
@@ -312,8 +327,21 @@ __device__ __forceinline__ void dma_tile(const HeadView &hv, const StepView &sv,
     for (int st = 0; st < NST; ++st) {
       wait_slices<WIW, SW - 2>(NST - 1 - st);
       block_barrier_no_vmem_wait();
-      if (st + SW - 1 < NST) issue_w(st + SW - 1);
-      compute(st);
+      const int cs = st + SW - 1;        // the slice whose copies go out now
+      const bool go = cs < NST;
+      int ks = cs + kskew;
+      ks = ks >= NST ? ks - NST : ks;
+      const uint32_t sb = wbase + (uint32_t)((cs % SW) * WST);
+      compute(st, [&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        // copies q with q * NMF / WIW == m go out after MFMA m
+        static_for<0, WIW>([&](auto qc) __attribute__((always_inline)) {
+          constexpr int q = decltype(qc)::value;
+          if constexpr (q * NMF / WIW == m) {
+            if (go) lds_copy16_stream(src[q] + ks * SK, sb + (uint32_t)((wave_s * WIW + q) * 1024));
+          }
+        });
+      });
     }
   } else {
     // unrolled by HL, so that each register buffer has a fixed name: buffer j
@@ -321,11 +349,26 @@ __device__ __forceinline__ void dma_tile(const HeadView &hv, const StepView &sv,
     auto iteration = [&](int st, u32x4 (&hbj)[AIA]) __attribute__((always_inline)) {
       wait_vmem_and_lds<63>();
       block_barrier_no_vmem_wait();
-      store_a(st + SA - 1, hbj);        // into the stage read in iteration st - 1
-      // the loads reuse the registers just stored: keep them after the stores
-      __builtin_amdgcn_sched_barrier(0);
-      load_a(st + SA - 1 + HL, hbj);
-      compute(st);
+      const int ss = st + SA - 1;        // stored now, into the stage read in iteration st - 1
+      const bool sgo = ss < NST;
+      char *sbase = aring + (ss % SA) * AST + ((wave_s - 2) * AIA) * 1024 + lane * 16;
+      int ks = min(st + SA - 1 + HL, NST - 1) + kskew;
+      ks = ks >= NST ? ks - NST : ks;
+      compute(st, [&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        // op o < AIA: store chunk o; op AIA + q: reload register q (after its store)
+        static_for<0, 2 * AIA>([&](auto oc) __attribute__((always_inline)) {
+          constexpr int o = decltype(oc)::value;
+          if constexpr (o * NMF / (2 * AIA) == m) {
+            if constexpr (o < AIA) {
+              if (sgo) *reinterpret_cast<u32x4 *>(sbase + o * 1024) = hbj[o];
+            } else {
+              constexpr int q = o - AIA;
+              hbj[q] = *reinterpret_cast<const u32x4 *>(src[q] + ks * SK);
+            }
+          }
+        });
+      });
     };
     int st0 = 0;
     for (; st0 + HL <= NST; st0 += HL) {
