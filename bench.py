@@ -639,8 +639,8 @@ def main():
     roof.update(traffic=k1_traffic(wl.name), kernel="head_gemm (mcd_head_logits)",
                 us_per_launch=round(ms_k1 * 1e3, 2),
                 measured="HIP events around back-to-back projection launches over the "
-                         "timed steps (in-step events add command-processor time per "
-                         "event: step.split_events)",
+                         "timed steps (in-step events can add command-processor time: "
+                         "step.split_events)",
                 algorithmic_bytes=alg["bytes"], algorithmic_flops=alg["flops"])
     out = {
         "metric": "codebook tokens/sec per CFG-paired decode step",
